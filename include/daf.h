@@ -1,0 +1,208 @@
+/*
+ * daf.h - C ABI of the Decoupled Attention Fusion (DAF) per-layer prefill
+ * attention library for AMD Instinct MI355X (gfx950).
+ *
+ * DAF (Sec. 2 of the paper) replaces full prefill attention over retrieved
+ * documents whose KV caches were computed offline, one document at a time, by
+ * three stages per layer:
+ *   1. important-token self-attention: the n = r*L_d important tokens are
+ *      gathered from all documents into a condensed sequence and attend only to
+ *      each other (Sec. 2 item 1; Complexity Analysis);
+ *   2. question-document attention: the L_q question tokens, at the tail of the
+ *      sequence, attend over all L_d + L_q keys, reading a hybrid KV cache in
+ *      which the important tokens' rows already hold their recomputed K/V
+ *      (Sec. 2 item 2);
+ *   3. state fusion: the outputs of both stages are written into the layer's
+ *      hidden states (Sec. 2 item 3).
+ * The selection policy that picks the important tokens and the Q/K/V
+ * projections stay with the caller: indices and projected Q/K/V are inputs.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory. Every tensor pointer is DEVICE memory owned by the caller; the
+ *   library allocates and frees nothing. Scratch memory comes from the caller's
+ *   `workspace`. Pointers must be 16-byte aligned.
+ * Layouts. Tensors are token-major and contiguous: queries and outputs are
+ *   [tokens][Hq][D], keys and values [tokens][Hkv][D], elements of `dtype`.
+ *   One output row (Hq*D elements) is one row of the hidden-state buffer.
+ *   LSE outputs are float32 [Hq][rows] (natural log of the softmax
+ *   denominator, including the max), row = the output's token row.
+ * Requests. A call serves a ragged batch of B >= 1 independent requests
+ *   (daf_batch_t). Request b has L_d,b document tokens, L_q,b question tokens
+ *   and n_b important tokens. Its rows are:
+ *     important rows (q_imp, k_imp, v_imp, o_imp, idx): cu_imp[b] .. cu_imp[b+1]
+ *     question rows  (q_q, k_q, v_q, o_q):              cu_q[b]   .. cu_q[b+1]
+ *     token rows     (k_cache, v_cache, hidden):        tok_b .. tok_b + T_b,
+ *       tok_b = cu_doc[b] + cu_q[b], T_b = L_d,b + L_q,b, documents first.
+ * Indices. idx[cu_imp[b] + i] is the request-local original position of
+ *   request b's i-th important token: 0 <= idx < L_d,b and strictly increasing
+ *   within a request. This is NOT checked on the hot path (violations are
+ *   undefined behaviour: duplicate rows make the scatters race);
+ *   daf_check_indices() verifies it on the device.
+ * Masks. Stage 1: important token i sees important token j iff j <= i (the
+ *   condensed order is the original order, so this is causal by original
+ *   position). Stage 2: question token j sees every document token and
+ *   question tokens 0..j.
+ * Numerics. bf16 or fp32 in; fp32 accumulation and softmax; outputs in the
+ *   input dtype. bf16 attention rounds the softmax probabilities to bf16
+ *   before the value product.
+ * Asynchrony. Work is enqueued on `stream` (NULL = the default stream) and the
+ *   call returns without synchronising. There is no global state: calls are
+ *   re-entrant; calls that write the same buffers must be ordered by the
+ *   caller.
+ * Errors. Every host-visible precondition is checked before anything is
+ *   enqueued; on failure the call returns a non-zero daf_status_t, enqueues
+ *   nothing, and daf_last_error() describes the problem (thread-local). A
+ *   failed kernel launch returns DAF_ERR_HIP. No C++ exception crosses the ABI.
+ */
+#ifndef DAF_H_
+#define DAF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DAF_OK = 0,
+  DAF_ERR_INVALID_ARG = 1, /* null pointer, bad size, inconsistent offsets */
+  DAF_ERR_ALIGNMENT = 2,   /* pointer or row size not a multiple of 16 bytes */
+  DAF_ERR_UNSUPPORTED = 3, /* head_dim / dtype the kernels do not cover */
+  DAF_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required */
+  DAF_ERR_HIP = 5          /* a HIP runtime call or kernel launch failed */
+} daf_status_t;
+
+typedef enum { DAF_BF16 = 0, DAF_F32 = 1 } daf_dtype_t;
+
+/* Attention shape. Query head h reads key/value head h / (Hq / Hkv). */
+typedef struct {
+  int32_t n_q_heads;   /* Hq >= 1 */
+  int32_t n_kv_heads;  /* Hkv >= 1, divides Hq */
+  int32_t head_dim;    /* D: 64 or 128 */
+  int32_t dtype;       /* daf_dtype_t of every tensor */
+  float softmax_scale; /* > 0, or 0 for 1/sqrt(D) */
+} daf_attn_cfg_t;
+
+/* Ragged batch. All three arrays are HOST memory, [batch + 1] prefix sums
+ * starting at 0: cu_doc of L_d,b, cu_q of L_q,b, cu_imp of n_b (n_b <= L_d,b).
+ * The library reads them during the call only. */
+typedef struct {
+  int32_t batch;
+  const int32_t *cu_doc;
+  const int32_t *cu_q;
+  const int32_t *cu_imp;
+} daf_batch_t;
+
+/* daf_gather_important `src_layout` values. */
+enum {
+  DAF_SRC_TOKENS = 0, /* src has T_b rows per request starting at tok_b */
+  DAF_SRC_DOCS = 1    /* src has L_d,b rows per request starting at cu_doc[b] */
+};
+
+/* daf_fuse `flags` bits. */
+enum {
+  DAF_FUSE_KV = 1,    /* hybrid KV cache + question KV append */
+  DAF_FUSE_HIDDEN = 2 /* stage outputs into the hidden states */
+};
+
+/* Gather the important rows into a condensed sequence (Sec. 2 item 1: the
+ * important tokens of all documents are gathered into one condensed
+ * sequence).
+ *   dst[cu_imp[b] + i] = src[base_b + idx[cu_imp[b] + i]]   (row_bytes each)
+ * with base_b = tok_b for DAF_SRC_TOKENS or cu_doc[b] for DAF_SRC_DOCS. Rows
+ * are copied bit for bit; row_bytes must be a positive multiple of 16. Used
+ * for the hidden rows that feed the caller's QKV projection and for K/V rows
+ * of a full-length cache. */
+daf_status_t daf_gather_important(const daf_batch_t *batch, int32_t src_layout,
+                                  const void *src, int64_t row_bytes,
+                                  const int32_t *idx, void *dst,
+                                  hipStream_t stream);
+
+/* Stage 1, important-token self-attention (Sec. 2 item 1; Complexity
+ * Analysis: important tokens attend only to each other, O(r^2 L_d^2)).
+ *   q_imp [sum n][Hq][D], k_imp / v_imp [sum n][Hkv][D] -> o_imp [sum n][Hq][D]
+ *   lse_imp: nullable float32 [Hq][sum n].
+ * Within request b, row i attends rows 0..i of the same request (causal in the
+ * condensed order, which is the original order). */
+daf_status_t daf_imp_self_attn(const daf_attn_cfg_t *cfg,
+                               const daf_batch_t *batch, const void *q_imp,
+                               const void *k_imp, const void *v_imp,
+                               void *o_imp, float *lse_imp, hipStream_t stream);
+
+/* Bytes of workspace daf_qdoc_attn needs for this shape (0 on bad input). */
+size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg,
+                               const daf_batch_t *batch);
+
+/* Stage 2, question-document attention (Sec. 2 item 2: an L_q x (L_d + L_q)
+ * attention over the hybrid KV cache; Complexity Analysis: O(L_q (L_d+L_q))).
+ *   q_q [sum L_q][Hq][D]; k_cache / v_cache hold T_b token rows per request
+ *   (the hybrid cache: daf_fuse(DAF_FUSE_KV) first) -> o_q [sum L_q][Hq][D];
+ *   lse_q: nullable float32 [Hq][sum L_q].
+ * Question row j of request b attends cache rows 0 .. L_d,b + j. The keys are
+ * split across workgroups; partial results live in `workspace` (at least
+ * daf_qdoc_workspace_size bytes, 16-byte aligned, contents undefined after
+ * the call) and are merged by log-sum-exp. */
+daf_status_t daf_qdoc_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
+                           const void *q_q, const void *k_cache,
+                           const void *v_cache, void *o_q, float *lse_q,
+                           void *workspace, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* State fusion and hybrid-cache construction, as in-place row scatters (Sec. 2
+ * item 2: the important tokens' K/V are updated in the document cache before
+ * question-document attention; Sec. 2 item 3: stage outputs are fused into the
+ * hidden states).
+ * DAF_FUSE_KV (needs k_imp, v_imp, k_q, v_q, k_cache, v_cache):
+ *   k_cache[tok_b + idx[.]] = k_imp[.],   k_cache[tok_b + L_d,b + j] = k_q[.]
+ *   (same for v) - the hybrid cache, with the question's K/V after the docs.
+ * DAF_FUSE_HIDDEN (needs o_imp, o_q, hidden [sum T][Hq*D]):
+ *   hidden[tok_b + idx[.]] = o_imp[.],    hidden[tok_b + L_d,b + j] = o_q[.]
+ * Rows are copied bit for bit; every other row is left untouched. Pointers not
+ * needed by the selected flags may be NULL. */
+daf_status_t daf_fuse(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
+                      uint32_t flags, const int32_t *idx, const void *k_imp,
+                      const void *v_imp, const void *k_q, const void *v_q,
+                      void *k_cache, void *v_cache, const void *o_imp,
+                      const void *o_q, void *hidden, hipStream_t stream);
+
+/* Bytes of workspace daf_layer_attn needs (0 on bad input). */
+size_t daf_layer_workspace_size(const daf_attn_cfg_t *cfg,
+                                const daf_batch_t *batch);
+
+/* One DAF attention layer (Sec. 2 items 1-3), in the order the paper fixes:
+ * hybrid KV write-back (DAF_FUSE_KV), stage 1, stage 2, then
+ * DAF_FUSE_HIDDEN, all on `stream`. Arguments as in the stage calls; o_imp and
+ * o_q receive the stage outputs as well as being fused into `hidden`. */
+daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
+                            const int32_t *idx, const void *q_imp,
+                            const void *k_imp, const void *v_imp,
+                            const void *q_q, const void *k_q, const void *v_q,
+                            void *k_cache, void *v_cache, void *o_imp,
+                            float *lse_imp, void *o_q, float *lse_q,
+                            void *hidden, void *workspace, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Debug check of the index precondition: writes to *d_bad_count (device
+ * int32) the number of entries of idx that are out of [0, L_d,b) or not
+ * greater than their predecessor in the same request. */
+daf_status_t daf_check_indices(const daf_batch_t *batch, const int32_t *idx,
+                               int32_t *d_bad_count, hipStream_t stream);
+
+/* Static name of a status code. */
+const char *daf_status_string(daf_status_t status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *daf_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t daf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DAF_H_ */

@@ -1,0 +1,559 @@
+// DAF C ABI: argument validation, launch planning and the one-layer driver.
+// Every check runs on the host before anything is enqueued; the kernels live
+// in attn.hip and rows.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "daf.h"
+#include "daf_internal.h"
+
+namespace {
+
+using namespace daf;
+
+thread_local char g_err[512] = "";
+
+daf_status_t fail(daf_status_t st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+daf_status_t ok() {
+  g_err[0] = '\0';
+  return DAF_OK;
+}
+
+daf_status_t hip_fail(hipError_t e, const char *what) {
+  return fail(DAF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct Cfg {
+  int hq, hkv, group, d, dtype;
+  float scale;
+  int elem;    // bytes per element
+  int key_tile;
+};
+
+struct Req {
+  int L_d, L_q, n;
+  int imp0, q0;
+  int64_t tok0;  // first token row (cache / hidden)
+};
+
+struct Batch {
+  std::vector<Req> r;
+  int64_t total_imp = 0, total_q = 0, total_tok = 0;
+};
+
+daf_status_t parse_cfg(const daf_attn_cfg_t *c, Cfg &out) {
+  if (!c) return fail(DAF_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->n_q_heads < 1 || c->n_kv_heads < 1)
+    return fail(DAF_ERR_INVALID_ARG, "head counts must be >= 1 (Hq=%d, Hkv=%d)", c->n_q_heads,
+                c->n_kv_heads);
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(DAF_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", c->n_q_heads, c->n_kv_heads);
+  if (c->n_q_heads > 1024) return fail(DAF_ERR_UNSUPPORTED, "Hq=%d exceeds 1024", c->n_q_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(DAF_ERR_UNSUPPORTED, "head_dim=%d (supported: 64, 128)", c->head_dim);
+  if (c->dtype != DAF_BF16 && c->dtype != DAF_F32)
+    return fail(DAF_ERR_UNSUPPORTED, "dtype=%d (supported: DAF_BF16, DAF_F32)", c->dtype);
+  if (!(c->softmax_scale >= 0.f) || !isfinite(c->softmax_scale))
+    return fail(DAF_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
+  out.hq = c->n_q_heads;
+  out.hkv = c->n_kv_heads;
+  out.group = out.hq / out.hkv;
+  out.d = c->head_dim;
+  out.dtype = c->dtype;
+  out.scale = c->softmax_scale > 0.f ? c->softmax_scale : 1.f / sqrtf((float)c->head_dim);
+  out.elem = c->dtype == DAF_BF16 ? 2 : 4;
+  out.key_tile = c->dtype == DAF_BF16 ? 64 : 32;
+  return DAF_OK;
+}
+
+daf_status_t parse_batch(const daf_batch_t *b, Batch &out) {
+  if (!b) return fail(DAF_ERR_INVALID_ARG, "batch is NULL");
+  if (b->batch < 1) return fail(DAF_ERR_INVALID_ARG, "batch=%d must be >= 1", b->batch);
+  if (!b->cu_doc || !b->cu_q || !b->cu_imp)
+    return fail(DAF_ERR_INVALID_ARG, "cu_doc, cu_q and cu_imp must be non-NULL host arrays");
+  if (b->cu_doc[0] != 0 || b->cu_q[0] != 0 || b->cu_imp[0] != 0)
+    return fail(DAF_ERR_INVALID_ARG, "prefix arrays must start at 0");
+  out.r.resize(b->batch);
+  int64_t tok = 0;
+  for (int i = 0; i < b->batch; ++i) {
+    Req &q = out.r[i];
+    q.L_d = b->cu_doc[i + 1] - b->cu_doc[i];
+    q.L_q = b->cu_q[i + 1] - b->cu_q[i];
+    q.n = b->cu_imp[i + 1] - b->cu_imp[i];
+    if (q.L_d < 0 || q.L_q < 0 || q.n < 0)
+      return fail(DAF_ERR_INVALID_ARG, "request %d: prefix arrays must be non-decreasing", i);
+    if (q.n > q.L_d)
+      return fail(DAF_ERR_INVALID_ARG, "request %d: n=%d important tokens exceed L_d=%d", i, q.n, q.L_d);
+    q.imp0 = b->cu_imp[i];
+    q.q0 = b->cu_q[i];
+    q.tok0 = tok;
+    tok += (int64_t)q.L_d + q.L_q;
+  }
+  if (tok > INT32_MAX) return fail(DAF_ERR_UNSUPPORTED, "total token rows %lld exceed 2^31-1", (long long)tok);
+  out.total_imp = b->cu_imp[b->batch];
+  out.total_q = b->cu_q[b->batch];
+  out.total_tok = tok;
+  return DAF_OK;
+}
+
+daf_status_t need_ptr(const void *p, const char *name) {
+  if (!p) return fail(DAF_ERR_INVALID_ARG, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+    return fail(DAF_ERR_ALIGNMENT, "%s is not 16-byte aligned", name);
+  return DAF_OK;
+}
+
+#define CHECK(expr)                   \
+  do {                                \
+    daf_status_t st_ = (expr);        \
+    if (st_ != DAF_OK) return st_;    \
+  } while (0)
+
+// ---- stage-2 split plan (depends on the shape only) --------------------------
+struct Split {
+  int n_splits, split_keys;
+};
+
+std::vector<Split> plan_splits(const Cfg &c, const Batch &b) {
+  const int BN = c.key_tile;
+  double work = 0;
+  for (const Req &q : b.r) {
+    if (q.L_q == 0) continue;
+    const int mbs = (q.L_q + kAttnBM - 1) / kAttnBM;
+    const int kbs = (q.L_d + q.L_q + BN - 1) / BN;
+    work += (double)c.hq * mbs * kbs;
+  }
+  const double per_wg = std::max(1.0, work / kTargetWorkgroups);
+  std::vector<Split> out(b.r.size());
+  for (size_t i = 0; i < b.r.size(); ++i) {
+    const Req &q = b.r[i];
+    const int kbs = std::max(1, (q.L_d + q.L_q + BN - 1) / BN);
+    int s = (int)std::lround(kbs / per_wg);
+    s = std::min(std::max(s, 1), kbs);
+    const int blocks = (kbs + s - 1) / s;
+    out[i].split_keys = blocks * BN;
+    out[i].n_splits = (kbs + blocks - 1) / blocks;
+  }
+  return out;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct WsLayout {
+  size_t part_o_bytes, part_lse_bytes, total;
+  int64_t part_rows;  // sum over requests of L_q * n_splits
+};
+
+WsLayout ws_layout(const Cfg &c, const Batch &b, const std::vector<Split> &sp) {
+  WsLayout w{};
+  w.part_rows = 0;
+  for (size_t i = 0; i < b.r.size(); ++i) w.part_rows += (int64_t)b.r[i].L_q * sp[i].n_splits;
+  w.part_o_bytes = align_up((size_t)w.part_rows * c.hq * c.d * sizeof(float));
+  w.part_lse_bytes = align_up((size_t)w.part_rows * c.hq * sizeof(float));
+  w.total = w.part_o_bytes + w.part_lse_bytes;
+  return w;
+}
+
+// ---- attention work tables ----------------------------------------------------
+AttnEntry self_entry(const Cfg &c, const Req &q, int64_t total_imp, const void *q_imp,
+                     const void *k_imp, const void *v_imp, void *o_imp, float *lse_imp) {
+  AttnEntry e{};
+  const size_t qrow = (size_t)c.hq * c.d * c.elem, krow = (size_t)c.hkv * c.d * c.elem;
+  e.q = static_cast<const char *>(q_imp) + q.imp0 * qrow;
+  e.k = static_cast<const char *>(k_imp) + q.imp0 * krow;
+  e.v = static_cast<const char *>(v_imp) + q.imp0 * krow;
+  e.o = static_cast<char *>(o_imp) + q.imp0 * qrow;
+  e.lse = lse_imp ? lse_imp + q.imp0 : nullptr;
+  e.lse_stride = (int32_t)total_imp;
+  e.n_rows = q.n;
+  e.n_keys = q.n;
+  const int mbs = (q.n + kAttnBM - 1) / kAttnBM;
+  e.mb_hi = mbs - 1;
+  e.mb_count = mbs;
+  e.n_splits = 1;
+  e.split_keys = (q.n + c.key_tile - 1) / c.key_tile * c.key_tile;
+  return e;
+}
+
+AttnEntry qdoc_entry(const Cfg &c, const Req &q, const Split &sp, int64_t part_row0,
+                     const void *q_q, const void *k_cache, const void *v_cache, float *part_o,
+                     float *part_lse) {
+  AttnEntry e{};
+  const size_t qrow = (size_t)c.hq * c.d * c.elem, krow = (size_t)c.hkv * c.d * c.elem;
+  e.q = static_cast<const char *>(q_q) + q.q0 * qrow;
+  e.k = static_cast<const char *>(k_cache) + q.tok0 * krow;
+  e.v = static_cast<const char *>(v_cache) + q.tok0 * krow;
+  e.o = nullptr;
+  e.lse = nullptr;
+  e.part_o = part_o + part_row0 * c.hq * c.d;
+  e.part_lse = part_lse + part_row0 * c.hq;
+  e.n_rows = q.L_q;
+  e.n_keys = q.L_d + q.L_q;
+  const int mbs = (q.L_q + kAttnBM - 1) / kAttnBM;
+  e.mb_hi = mbs - 1;
+  e.mb_count = mbs;
+  e.n_splits = sp.n_splits;
+  e.split_keys = sp.split_keys;
+  return e;
+}
+
+int entry_groups(const Cfg &c, const AttnEntry &e) { return e.mb_count * e.n_splits * c.hkv; }
+
+daf_status_t run_entries(const Cfg &c, AttnKind kind, std::vector<AttnEntry> &entries, hipStream_t st) {
+  for (size_t i0 = 0; i0 < entries.size(); i0 += kMaxEntries) {
+    AttnLaunch p{};
+    p.hq = c.hq;
+    p.hkv = c.hkv;
+    p.group = c.group;
+    p.scale_log2 = c.scale * 1.4426950408889634f;
+    int groups = 0;
+    const size_t i1 = std::min(entries.size(), i0 + kMaxEntries);
+    for (size_t i = i0; i < i1; ++i) {
+      AttnEntry e = entries[i];
+      e.group0 = groups;
+      groups += entry_groups(c, e);
+      p.e[p.n_entries++] = e;
+    }
+    p.n_groups = groups;
+    hipError_t err = launch_attention(c.dtype, c.d, kind, p, st);
+    if (err != hipSuccess) return hip_fail(err, "attention launch");
+  }
+  return DAF_OK;
+}
+
+void add_self_entries(const Cfg &c, const Batch &b, const void *q_imp, const void *k_imp,
+                      const void *v_imp, void *o_imp, float *lse_imp, std::vector<AttnEntry> &out) {
+  // heaviest requests first: their top query blocks carry the most work
+  std::vector<int> order;
+  for (int i = 0; i < (int)b.r.size(); ++i)
+    if (b.r[i].n > 0) order.push_back(i);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return b.r[x].n > b.r[y].n; });
+  for (int i : order) out.push_back(self_entry(c, b.r[i], b.total_imp, q_imp, k_imp, v_imp, o_imp, lse_imp));
+}
+
+daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const void *k_cache,
+                          const void *v_cache, void *workspace, size_t ws_bytes,
+                          std::vector<AttnEntry> &out, std::vector<MergeEntry> &merge, void *o_q,
+                          float *lse_q) {
+  const std::vector<Split> sp = plan_splits(c, b);
+  const WsLayout w = ws_layout(c, b, sp);
+  if (w.part_rows == 0) return DAF_OK;
+  if (!workspace) return fail(DAF_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", w.total);
+  if (ws_bytes < w.total) return fail(DAF_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, w.total);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+    return fail(DAF_ERR_ALIGNMENT, "workspace is not 16-byte aligned");
+  float *part_o = static_cast<float *>(workspace);
+  float *part_lse = reinterpret_cast<float *>(static_cast<char *>(workspace) + w.part_o_bytes);
+  int64_t prow = 0;
+  const size_t qrow = (size_t)c.hq * c.d * c.elem;
+  for (size_t i = 0; i < b.r.size(); ++i) {
+    const Req &q = b.r[i];
+    if (q.L_q == 0) continue;
+    out.push_back(qdoc_entry(c, q, sp[i], prow, q_q, k_cache, v_cache, part_o, part_lse));
+    MergeEntry m{};
+    m.part_o = part_o + prow * c.hq * c.d;
+    m.part_lse = part_lse + prow * c.hq;
+    m.o = static_cast<char *>(o_q) + q.q0 * qrow;
+    m.lse = lse_q ? lse_q + q.q0 : nullptr;
+    m.lse_stride = (int32_t)b.total_q;
+    m.n_rows = q.L_q;
+    m.n_splits = sp[i].n_splits;
+    merge.push_back(m);
+    prow += (int64_t)q.L_q * sp[i].n_splits;
+  }
+  return DAF_OK;
+}
+
+daf_status_t run_merge(const Cfg &c, std::vector<MergeEntry> &merge, hipStream_t st) {
+  for (size_t i0 = 0; i0 < merge.size(); i0 += kMaxEntries) {
+    MergeLaunch p{};
+    p.hq = c.hq;
+    int rows = 0;
+    const size_t i1 = std::min(merge.size(), i0 + kMaxEntries);
+    for (size_t i = i0; i < i1; ++i) {
+      MergeEntry m = merge[i];
+      m.row0 = rows;
+      rows += m.n_rows;
+      p.e[p.n_entries++] = m;
+    }
+    p.total_rows = rows;
+    hipError_t err = launch_merge(c.dtype, c.d, p, st);
+    if (err != hipSuccess) return hip_fail(err, "merge launch");
+  }
+  return DAF_OK;
+}
+
+// ---- row movement ---------------------------------------------------------------
+template <typename F>
+daf_status_t for_row_groups(const Batch &b, const int32_t *idx, int64_t row_bytes, int layout_docs,
+                            F &&fn) {
+  const int nreq = (int)b.r.size();
+  for (int i0 = 0; i0 < nreq; i0 += kMaxRowReqs) {
+    RowLaunch p{};
+    p.units = (int32_t)(row_bytes / 16);
+    p.idx = idx;
+    const int i1 = std::min(nreq, i0 + kMaxRowReqs);
+    int64_t cu_doc = 0;
+    for (int i = 0; i < i0; ++i) cu_doc += b.r[i].L_d;
+    for (int i = i0; i < i1; ++i) {
+      const Req &q = b.r[i];
+      RowReq &r = p.r[p.n_req++];
+      r.base = layout_docs ? cu_doc : q.tok0;
+      r.imp0 = q.imp0;
+      r.n_imp = q.n;
+      r.q0 = q.q0;
+      r.n_q = q.L_q;
+      r.L_d = q.L_d;
+      p.total_imp += q.n;
+      p.total_q += q.L_q;
+      cu_doc += q.L_d;
+    }
+    CHECK(fn(p));
+  }
+  return DAF_OK;
+}
+
+daf_status_t fuse_impl(const Cfg &c, const Batch &b, uint32_t flags, const int32_t *idx,
+                       const void *k_imp, const void *v_imp, const void *k_q, const void *v_q,
+                       void *k_cache, void *v_cache, const void *o_imp, const void *o_q, void *hidden,
+                       hipStream_t st) {
+  if (flags & DAF_FUSE_KV) {
+    ScatterPair pr[2] = {{k_imp, k_q, k_cache}, {v_imp, v_q, v_cache}};
+    CHECK(for_row_groups(b, idx, (int64_t)c.hkv * c.d * c.elem, 0, [&](const RowLaunch &p) {
+      hipError_t e = launch_scatter(p, pr, 2, st);
+      return e == hipSuccess ? DAF_OK : hip_fail(e, "KV fuse launch");
+    }));
+  }
+  if (flags & DAF_FUSE_HIDDEN) {
+    ScatterPair pr[1] = {{o_imp, o_q, hidden}};
+    CHECK(for_row_groups(b, idx, (int64_t)c.hq * c.d * c.elem, 0, [&](const RowLaunch &p) {
+      hipError_t e = launch_scatter(p, pr, 1, st);
+      return e == hipSuccess ? DAF_OK : hip_fail(e, "hidden fuse launch");
+    }));
+  }
+  return DAF_OK;
+}
+
+daf_status_t check_fuse_ptrs(const Batch &b, uint32_t flags, const int32_t *idx, const void *k_imp,
+                             const void *v_imp, const void *k_q, const void *v_q, void *k_cache,
+                             void *v_cache, const void *o_imp, const void *o_q, void *hidden) {
+  if ((flags & ~(uint32_t)(DAF_FUSE_KV | DAF_FUSE_HIDDEN)) != 0 || flags == 0)
+    return fail(DAF_ERR_INVALID_ARG, "flags=%u (use DAF_FUSE_KV and/or DAF_FUSE_HIDDEN)", flags);
+  const bool imp = b.total_imp > 0, qs = b.total_q > 0;
+  if (imp) CHECK(need_ptr(idx, "idx"));
+  if (flags & DAF_FUSE_KV) {
+    if (imp) {
+      CHECK(need_ptr(k_imp, "k_imp"));
+      CHECK(need_ptr(v_imp, "v_imp"));
+    }
+    if (qs) {
+      CHECK(need_ptr(k_q, "k_q"));
+      CHECK(need_ptr(v_q, "v_q"));
+    }
+    if (imp || qs) {
+      CHECK(need_ptr(k_cache, "k_cache"));
+      CHECK(need_ptr(v_cache, "v_cache"));
+    }
+  }
+  if (flags & DAF_FUSE_HIDDEN) {
+    if (imp) CHECK(need_ptr(o_imp, "o_imp"));
+    if (qs) CHECK(need_ptr(o_q, "o_q"));
+    if (imp || qs) CHECK(need_ptr(hidden, "hidden"));
+  }
+  return DAF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *daf_status_string(daf_status_t s) {
+  switch (s) {
+    case DAF_OK: return "DAF_OK";
+    case DAF_ERR_INVALID_ARG: return "DAF_ERR_INVALID_ARG";
+    case DAF_ERR_ALIGNMENT: return "DAF_ERR_ALIGNMENT";
+    case DAF_ERR_UNSUPPORTED: return "DAF_ERR_UNSUPPORTED";
+    case DAF_ERR_WORKSPACE: return "DAF_ERR_WORKSPACE";
+    case DAF_ERR_HIP: return "DAF_ERR_HIP";
+  }
+  return "DAF_ERR_UNKNOWN";
+}
+
+const char *daf_last_error(void) { return g_err; }
+
+int32_t daf_version(void) { return 100; }
+
+daf_status_t daf_gather_important(const daf_batch_t *batch, int32_t src_layout, const void *src,
+                                  int64_t row_bytes, const int32_t *idx, void *dst,
+                                  hipStream_t stream) {
+  try {
+    Batch b;
+    CHECK(parse_batch(batch, b));
+    if (src_layout != DAF_SRC_TOKENS && src_layout != DAF_SRC_DOCS)
+      return fail(DAF_ERR_INVALID_ARG, "src_layout=%d", src_layout);
+    if (row_bytes <= 0) return fail(DAF_ERR_INVALID_ARG, "row_bytes=%lld must be > 0", (long long)row_bytes);
+    if (row_bytes % 16 != 0) return fail(DAF_ERR_ALIGNMENT, "row_bytes=%lld is not a multiple of 16", (long long)row_bytes);
+    if (row_bytes / 16 > INT32_MAX) return fail(DAF_ERR_UNSUPPORTED, "row_bytes too large");
+    if (b.total_imp == 0) return ok();
+    CHECK(need_ptr(src, "src"));
+    CHECK(need_ptr(idx, "idx"));
+    CHECK(need_ptr(dst, "dst"));
+    CHECK(for_row_groups(b, idx, row_bytes, src_layout == DAF_SRC_DOCS, [&](const RowLaunch &p) {
+      hipError_t e = launch_gather(p, 0, src, dst, stream);
+      return e == hipSuccess ? DAF_OK : hip_fail(e, "gather launch");
+    }));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_imp_self_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, const void *q_imp,
+                               const void *k_imp, const void *v_imp, void *o_imp, float *lse_imp,
+                               hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    if (b.total_imp == 0) return ok();
+    CHECK(need_ptr(q_imp, "q_imp"));
+    CHECK(need_ptr(k_imp, "k_imp"));
+    CHECK(need_ptr(v_imp, "v_imp"));
+    CHECK(need_ptr(o_imp, "o_imp"));
+    if (lse_imp) CHECK(need_ptr(lse_imp, "lse_imp"));
+    std::vector<AttnEntry> entries;
+    add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, entries);
+    CHECK(run_entries(c, AttnKind::kSelf, entries, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg, const daf_batch_t *batch) {
+  try {
+    Cfg c;
+    Batch b;
+    if (parse_cfg(cfg, c) != DAF_OK || parse_batch(batch, b) != DAF_OK) return 0;
+    const WsLayout w = ws_layout(c, b, plan_splits(c, b));
+    return w.part_rows ? w.total : 0;
+  } catch (...) {
+    return 0;
+  }
+}
+
+size_t daf_layer_workspace_size(const daf_attn_cfg_t *cfg, const daf_batch_t *batch) {
+  return daf_qdoc_workspace_size(cfg, batch);
+}
+
+daf_status_t daf_qdoc_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, const void *q_q,
+                           const void *k_cache, const void *v_cache, void *o_q, float *lse_q,
+                           void *workspace, size_t ws_bytes, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    if (b.total_q == 0) return ok();
+    CHECK(need_ptr(q_q, "q_q"));
+    CHECK(need_ptr(k_cache, "k_cache"));
+    CHECK(need_ptr(v_cache, "v_cache"));
+    CHECK(need_ptr(o_q, "o_q"));
+    if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
+    std::vector<AttnEntry> entries;
+    std::vector<MergeEntry> merge;
+    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, entries, merge, o_q, lse_q));
+    CHECK(run_entries(c, AttnKind::kQdoc, entries, stream));
+    CHECK(run_merge(c, merge, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_fuse(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, uint32_t flags,
+                      const int32_t *idx, const void *k_imp, const void *v_imp, const void *k_q,
+                      const void *v_q, void *k_cache, void *v_cache, const void *o_imp,
+                      const void *o_q, void *hidden, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    CHECK(check_fuse_ptrs(b, flags, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, o_imp, o_q, hidden));
+    CHECK(fuse_impl(c, b, flags, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, o_imp, o_q, hidden, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, const int32_t *idx,
+                            const void *q_imp, const void *k_imp, const void *v_imp, const void *q_q,
+                            const void *k_q, const void *v_q, void *k_cache, void *v_cache,
+                            void *o_imp, float *lse_imp, void *o_q, float *lse_q, void *hidden,
+                            void *workspace, size_t ws_bytes, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    const uint32_t both = DAF_FUSE_KV | DAF_FUSE_HIDDEN;
+    if (b.total_imp == 0 && b.total_q == 0) return ok();
+    CHECK(check_fuse_ptrs(b, both, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, o_imp, o_q, hidden));
+    if (b.total_imp > 0) CHECK(need_ptr(q_imp, "q_imp"));
+    if (b.total_q > 0) CHECK(need_ptr(q_q, "q_q"));
+    if (lse_imp) CHECK(need_ptr(lse_imp, "lse_imp"));
+    if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
+    // plan (and check the workspace) before enqueueing anything
+    std::vector<AttnEntry> entries;
+    std::vector<MergeEntry> merge;
+    add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, entries);
+    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, entries, merge, o_q, lse_q));
+    // hybrid KV first (stage 2 reads it), then both attention stages in one
+    // grid, the split merge, and the fusion into the hidden states
+    CHECK(fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr, nullptr,
+                    nullptr, stream));
+    CHECK(run_entries(c, AttnKind::kLayer, entries, stream));
+    CHECK(run_merge(c, merge, stream));
+    CHECK(fuse_impl(c, b, DAF_FUSE_HIDDEN, idx, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                    o_imp, o_q, hidden, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_check_indices(const daf_batch_t *batch, const int32_t *idx, int32_t *d_bad_count,
+                               hipStream_t stream) {
+  try {
+    Batch b;
+    CHECK(parse_batch(batch, b));
+    CHECK(need_ptr(d_bad_count, "d_bad_count"));
+    if (b.total_imp > 0) CHECK(need_ptr(idx, "idx"));
+    int first = 1;
+    CHECK(for_row_groups(b, idx, 16, 0, [&](const RowLaunch &p) {
+      hipError_t e = launch_check_indices(p, d_bad_count, first ? 0 : 1, stream);
+      first = 0;
+      return e == hipSuccess ? DAF_OK : hip_fail(e, "check launch");
+    }));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+}  // extern "C"

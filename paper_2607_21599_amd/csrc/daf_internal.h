@@ -1,0 +1,105 @@
+// Internal declarations shared by the DAF HIP kernels and the host library.
+// gfx950 (MI355X) only: wave64, MFMA bf16 32x32x16, 8 XCDs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace daf {
+
+constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr int kAttnThreads = 256; // 4 waves, 32 query rows each
+constexpr int kAttnBM = 128;      // query rows per attention workgroup
+constexpr int kMaxEntries = 16;   // work-table entries per attention launch
+constexpr int kMaxRowReqs = 32;   // requests per row-movement launch
+constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident attention workgroups
+
+// One entry of an attention launch: one request of one stage, restricted to a
+// contiguous range of 128-row query blocks. Query row i (0-based in the
+// entry's request) sees keys 0 .. i + (n_keys - n_rows): causal, aligned to the
+// bottom right, which covers both DAF stages (stage 1: n_keys == n_rows;
+// stage 2: n_keys = L_d + L_q, n_rows = L_q).
+struct AttnEntry {
+  const void *q;   // [n_rows][Hq][D], row 0 of the request
+  const void *k;   // [n_keys][Hkv][D]
+  const void *v;
+  void *o;         // [n_rows][Hq][D] final output (direct mode), else null
+  float *lse;      // [Hq][lse_stride] at this request's first column, nullable
+  float *part_o;   // split mode: [n_rows * n_splits][Hq][D] fp32
+  float *part_lse; // split mode: [n_rows * n_splits][Hq]
+  int32_t lse_stride;
+  int32_t n_rows;
+  int32_t n_keys;
+  int32_t mb_hi;      // heaviest (last) query block of the range
+  int32_t mb_count;   // blocks mb_hi, mb_hi-1, ..., mb_hi-mb_count+1
+  int32_t n_splits;   // key splits (1 = direct mode)
+  int32_t split_keys; // keys per split, a multiple of the key tile
+  int32_t group0;     // first work group (G query heads sharing a KV head)
+};
+
+struct AttnLaunch {
+  int32_t hq, hkv, group;  // group = Hq / Hkv
+  int32_t n_entries;
+  int32_t n_groups;        // total work groups over all entries
+  float scale_log2;        // softmax scale * log2(e)
+  AttnEntry e[kMaxEntries];
+};
+
+// Log-sum-exp merge of split partials, one request per entry.
+struct MergeEntry {
+  const float *part_o;
+  const float *part_lse;
+  void *o;        // [n_rows][Hq][D]
+  float *lse;     // nullable, [Hq][lse_stride] at the request's first column
+  int32_t lse_stride;
+  int32_t n_rows;
+  int32_t n_splits;
+  int32_t row0;   // first global (row, head) item / Hq of this entry
+};
+
+struct MergeLaunch {
+  int32_t hq;
+  int32_t n_entries;
+  int32_t total_rows;
+  MergeEntry e[kMaxEntries];
+};
+
+// Row movement (gather / scatter), byte copies in 16-byte units.
+struct RowReq {
+  int64_t base;     // token-row base of the request in the full-length buffer
+  int32_t imp0;     // first important row / idx entry (cu_imp[b])
+  int32_t n_imp;
+  int32_t q0;       // first question row (cu_q[b])
+  int32_t n_q;
+  int32_t L_d;
+};
+
+struct RowLaunch {
+  int32_t n_req;
+  int32_t total_imp;  // sum of n_imp over these requests
+  int32_t total_q;    // sum of n_q (scatter only)
+  int32_t units;      // 16-byte units per row
+  const int32_t *idx; // full idx array (entries indexed by imp0 + i)
+  RowReq r[kMaxRowReqs];
+};
+
+struct ScatterPair {
+  const void *src_imp;  // [.][row] rows by important index
+  const void *src_q;    // [.][row] rows by question index
+  void *dst;            // full-length token rows
+};
+
+// Kernel launchers (defined in attn.hip / rows.hip). Return the launch error.
+enum class AttnKind { kSelf = 0, kQdoc = 1, kLayer = 2 };
+hipError_t launch_attention(int dtype, int head_dim, AttnKind kind,
+                            const AttnLaunch &p, hipStream_t s);
+hipError_t launch_merge(int dtype, int head_dim, const MergeLaunch &p,
+                        hipStream_t s);
+hipError_t launch_gather(const RowLaunch &p, int64_t src_base_unused,
+                         const void *src, void *dst, hipStream_t s);
+hipError_t launch_scatter(const RowLaunch &p, const ScatterPair *pairs,
+                          int n_pairs, hipStream_t s);
+hipError_t launch_check_indices(const RowLaunch &p, int32_t *d_bad,
+                                int accumulate, hipStream_t s);
+
+}  // namespace daf

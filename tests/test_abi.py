@@ -1,0 +1,120 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_21599_amd as daf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "daf.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(daf_[a-z_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = _declared()
+    assert len(names) >= 11
+    assert sorted(daf.EXPORTED) == names
+    lib = ctypes.CDLL(daf.library_path)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    assert daf.daf_status_string(0) == "DAF_OK"
+    assert daf.daf_status_string(5) == "DAF_ERR_HIP"
+    assert daf.daf_version() >= 100
+
+
+FAKE = 0x10000  # an aligned non-null address; never dereferenced on these paths
+
+
+def _cfg(**kw):
+    a = dict(n_q_heads=28, n_kv_heads=4, head_dim=128, dtype=daf.DAF_BF16, softmax_scale=0.0)
+    a.update(kw)
+    return daf.AttnCfg(**a)
+
+
+@pytest.mark.parametrize("cfg,status", [
+    (dict(n_kv_heads=3), daf.DAF_ERR_INVALID_ARG),
+    (dict(n_q_heads=0), daf.DAF_ERR_INVALID_ARG),
+    (dict(head_dim=96), daf.DAF_ERR_UNSUPPORTED),
+    (dict(dtype=7), daf.DAF_ERR_UNSUPPORTED),
+    (dict(softmax_scale=-1.0), daf.DAF_ERR_INVALID_ARG),
+    (dict(softmax_scale=float("nan")), daf.DAF_ERR_INVALID_ARG),
+])
+def test_bad_cfg(cfg, status):
+    b = daf.Batch.single(100, 8, 10)
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_imp_self_attn(_cfg(**cfg), b, FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == status
+    assert daf.daf_last_error()
+
+
+def test_bad_batches():
+    c = _cfg()
+    with pytest.raises(daf.DafError) as e:  # n > L_d
+        daf.daf_imp_self_attn(c, daf.Batch.single(10, 4, 11), FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # decreasing prefix
+        daf.daf_imp_self_attn(c, daf.Batch([0, 10, 5], [0, 1, 2], [0, 1, 2]), FAKE, FAKE, FAKE, FAKE,
+                              None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # prefix not starting at 0
+        daf.daf_imp_self_attn(c, daf.Batch([1, 10], [0, 1], [0, 1]), FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+
+
+def test_pointer_checks():
+    c = _cfg()
+    b = daf.Batch.single(100, 8, 10)
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_imp_self_attn(c, b, FAKE + 8, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_ALIGNMENT
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_imp_self_attn(c, b, None, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_gather_important(b, daf.DAF_SRC_TOKENS, FAKE, 24, FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_ALIGNMENT
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_gather_important(b, 5, FAKE, 32, FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_fuse(c, b, 0, FAKE, stream=0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # KV mode without the caches
+        daf.daf_fuse(c, b, daf.DAF_FUSE_KV, FAKE, k_imp=FAKE, v_imp=FAKE, k_q=FAKE, v_q=FAKE, stream=0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+
+
+def test_workspace_checks():
+    c = _cfg()
+    b = daf.Batch.single(32768, 128, 4915)
+    need = daf.daf_qdoc_workspace_size(c, b)
+    assert need == daf.daf_layer_workspace_size(c, b)
+    # 128 rows x 18 splits x 28 heads x (128 + 1) fp32, each region 256-byte aligned
+    assert need == 128 * 18 * 28 * 128 * 4 + ((128 * 18 * 28 * 4 + 255) // 256) * 256
+    for ws, nbytes, status in [(None, need, daf.DAF_ERR_WORKSPACE), (FAKE, need - 1, daf.DAF_ERR_WORKSPACE),
+                               (FAKE + 4, need, daf.DAF_ERR_ALIGNMENT)]:
+        with pytest.raises(daf.DafError) as e:
+            daf.daf_qdoc_attn(c, b, FAKE, FAKE, FAKE, FAKE, None, ws, nbytes, 0)
+        assert e.value.status == status
+    assert daf.daf_qdoc_workspace_size(_cfg(head_dim=96), b) == 0
+    assert daf.daf_qdoc_workspace_size(c, daf.Batch.single(100, 0, 3)) == 0
+
+
+def test_empty_work_is_a_no_op():
+    c = _cfg()
+    b = daf.Batch.single(0, 0, 0)
+    daf.daf_imp_self_attn(c, b, None, None, None, None, None, 0)
+    daf.daf_qdoc_attn(c, b, None, None, None, None, None, None, 0, 0)
+    daf.daf_layer_attn(c, b, *([None] * 14), None, 0, 0)
+    daf.daf_gather_important(b, daf.DAF_SRC_TOKENS, None, 16, None, None, 0)
