@@ -1,0 +1,223 @@
+"""Benchmark of the DAF per-layer prefill attention on one MI355X.
+
+One step is one pass of the whole hot path over one synthetic layer already
+resident in HBM: the important-row gather of the hidden states, then
+daf_layer_attn (hybrid KV write-back, stage 1 and stage 2 in one grid, split
+merge, fusion into the hidden states). W untimed warmup steps, then exactly K
+timed steps between device synchronisations. Several copies of the inputs are
+used in rotation so that consecutive steps do not find their data in the
+256 MB Infinity Cache.
+
+A second timed loop calls the stages one by one with HIP events between them
+(on the stream the kernels run on) for per-stage times, TFLOP/s, TB/s and the
+roofline fraction of the dominant kernel (stage 1). The CPU oracle is timed on
+the host on a bounded sample of the same layer (``cpu_baseline``).
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import daf_inputs as di  # noqa: E402
+
+METRIC = "DAF per-layer attention µs at L_d=32k,r=0.15; stage TFLOP/s + HBM TB/s vs peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def work(shapes) -> dict:
+    """Algorithmic FLOP and HBM bytes per stage (causal masks counted exactly,
+    every operand read once, every output written once)."""
+    f1 = f2 = b1 = b2 = bkv = bhid = bgat = 0
+    for s in shapes:
+        eb = 2 if s.dtype == di.BF16 else 4
+        qrow, krow = s.hq * s.d * eb, s.hkv * s.d * eb
+        f1 += 4 * s.d * s.hq * s.n * (s.n + 1) // 2
+        f2 += 4 * s.d * s.hq * (s.L_q * s.L_d + s.L_q * (s.L_q + 1) // 2)
+        b1 += s.n * (2 * qrow + 2 * krow)
+        b2 += s.T * 2 * krow + 2 * s.L_q * qrow
+        bkv += 2 * (s.n + s.L_q) * 2 * krow
+        bhid += 2 * (s.n + s.L_q) * qrow
+        bgat += 2 * s.n * qrow
+    return dict(stage1_flop=f1, stage2_flop=f2, stage1_bytes=b1, stage2_bytes=b2, fuse_kv_bytes=bkv,
+                fuse_hidden_bytes=bhid, gather_bytes=bgat)
+
+
+def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
+    """The oracle on every stride1-th stage-1 row and every stride2-th stage-2
+    row (plus the full hybrid-cache build and fusion), scaled to the layer."""
+    import oracle
+    orc = oracle.get()
+    w = di.raw_to_f32
+    t_total = 0.0
+    rows_done = [0, 0]
+    for b, s in enumerate(batch.shapes):
+        r = batch.request(b)
+        sc = oracle.default_scale(s.d)
+        rows1 = np.arange(0, s.n, stride1)
+        rows2 = np.arange(0, s.L_q, stride2)
+        q1, k1, v1 = w(r["q_imp"]), w(r["k_imp"]), w(r["v_imp"])
+        t0 = time.perf_counter()
+        kh, vh = orc.hybrid_kv(r["k_cache"], r["v_cache"], r["idx"], r["k_imp"], r["v_imp"], r["k_q"],
+                               r["v_q"], s.L_d)
+        t_hyb = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        o1, _ = orc.stage1(q1, k1, v1, r["idx"], sc, rows1)
+        t_s1 = time.perf_counter() - t0
+        kf, vf, qq = w(kh), w(vh), w(r["q_q"])
+        t0 = time.perf_counter()
+        o2, _ = orc.stage2(qq, kf, vf, s.L_d, sc, rows2)
+        t_s2 = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        orc.fuse_hidden(r["hidden"], r["idx"], r["q_imp"], r["q_q"], s.L_d)
+        t_fuse = time.perf_counter() - t0
+        t_total += t_hyb + t_fuse + t_s1 * s.n / max(1, len(rows1)) + t_s2 * s.L_q / max(1, len(rows2))
+        rows_done[0] += len(rows1)
+        rows_done[1] += len(rows2)
+    return dict(value=t_total * 1e6, unit="us", cores=orc.threads, kind="oracle",
+                sample=(f"stage-1 rows 0::{stride1} ({rows_done[0]} rows) and stage-2 rows 0::{stride2} "
+                        f"({rows_done[1]} rows) of every request, full hybrid-cache build and fusion; "
+                        "attention times scaled by total/sampled rows"))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen7b_32k")
+    ap.add_argument("--copies", type=int, default=3, help="input copies used in rotation")
+    ap.add_argument("--cpu-stride1", type=int, default=4)
+    ap.add_argument("--cpu-stride2", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (the DAF layer attention is measured on a "
+              "single MI355X); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_21599_amd as daf
+    from paper_2607_21599_amd.tensors import LayerBuffers
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    daf.lib()
+    shapes = di.workload(args.workload)
+    batch = di.make_batch(shapes)
+    s0 = shapes[0]
+    print(f"[bench] {args.workload}: generated inputs", file=sys.stderr, flush=True)
+    bufs = [LayerBuffers(batch.arrays, batch.cu_doc, batch.cu_q, batch.cu_imp, s0.hq, s0.hkv, s0.d)
+            for _ in range(max(1, args.copies))]
+    tdt = bufs[0]["hidden"].dtype
+    gath = [torch.empty((int(batch.cu_imp[-1]), s0.hq * s0.d), dtype=tdt, device="cuda") for _ in bufs]
+
+    def step(i):
+        j = i % len(bufs)
+        bufs[j].gather_hidden(gath[j])
+        bufs[j].layer()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(args.steps):
+        step(i)
+    t1.record()
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
+
+    # per-stage times: the same calls one by one, events on the launch stream
+    names = ["gather", "fuse_kv", "stage1", "stage2", "fuse_hidden"]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        b = bufs[i % len(bufs)]
+        g = gath[i % len(bufs)]
+        e = ev[i]
+        e[0].record()
+        b.gather_hidden(g)
+        e[1].record()
+        b.fuse_kv()
+        e[2].record()
+        b.stage1()
+        e[3].record()
+        b.stage2()
+        e[4].record()
+        b.fuse_hidden()
+        e[5].record()
+    torch.cuda.synchronize()
+    stage_us = {n: float(np.mean([ev[i][k].elapsed_time(ev[i][k + 1]) for i in range(args.steps)])) * 1e3
+                for k, n in enumerate(names)}
+    wk = work(shapes)
+    peak_mma = PEAK_BF16_TFLOPS if s0.dtype == di.BF16 else PEAK_F32_TFLOPS
+
+    def tflops(f, us):
+        return f / (us * 1e-6) / 1e12
+
+    def gbs(by, us):
+        return by / (us * 1e-6) / 1e9
+
+    stages = {
+        "gather": dict(us=stage_us["gather"], GBps=gbs(wk["gather_bytes"], stage_us["gather"]),
+                       bytes=wk["gather_bytes"]),
+        "fuse_kv": dict(us=stage_us["fuse_kv"], GBps=gbs(wk["fuse_kv_bytes"], stage_us["fuse_kv"]),
+                        bytes=wk["fuse_kv_bytes"]),
+        "stage1_imp_self_attn": dict(us=stage_us["stage1"], TFLOPs=tflops(wk["stage1_flop"], stage_us["stage1"]),
+                                     GBps=gbs(wk["stage1_bytes"], stage_us["stage1"]), flop=wk["stage1_flop"],
+                                     bytes=wk["stage1_bytes"]),
+        "stage2_qdoc_attn": dict(us=stage_us["stage2"], TFLOPs=tflops(wk["stage2_flop"], stage_us["stage2"]),
+                                 GBps=gbs(wk["stage2_bytes"], stage_us["stage2"]), flop=wk["stage2_flop"],
+                                 bytes=wk["stage2_bytes"]),
+        "fuse_hidden": dict(us=stage_us["fuse_hidden"],
+                            GBps=gbs(wk["fuse_hidden_bytes"], stage_us["fuse_hidden"]),
+                            bytes=wk["fuse_hidden_bytes"]),
+    }
+    for k in ("gather", "fuse_kv", "fuse_hidden"):
+        stages[k]["hbm_frac"] = stages[k]["GBps"] / PEAK_HBM_GBS
+    for k in ("stage1_imp_self_attn", "stage2_qdoc_attn"):
+        st = stages[k]
+        st["mfma_frac"] = st["TFLOPs"] / peak_mma
+        st["hbm_frac"] = st["GBps"] / PEAK_HBM_GBS
+        # roofline time of the bound that applies, over the measured time
+        t_floor = max(st["flop"] / (peak_mma * 1e12), st["bytes"] / (PEAK_HBM_GBS * 1e9))
+        st["roofline_frac"] = t_floor / (st["us"] * 1e-6)
+    s1 = stages["stage1_imp_self_attn"]
+    roofline = dict(bound="mfma", kernel="attn_fwd_kernel (stage 1, daf_imp_self_attn)",
+                    achieved=s1["TFLOPs"], peak=peak_mma, unit="TFLOP/s", frac=s1["TFLOPs"] / peak_mma,
+                    traffic=None, flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
+
+    out = {
+        "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if s0.dtype == di.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "L_d": [s.L_d for s in shapes] if len(shapes) > 1 else s0.L_d,
+                   "L_q": [s.L_q for s in shapes] if len(shapes) > 1 else s0.L_q,
+                   "n_imp": [s.n for s in shapes] if len(shapes) > 1 else s0.n,
+                   "q_heads": s0.hq, "kv_heads": s0.hkv, "head_dim": s0.d, "requests": len(shapes),
+                   "step": "gather + daf_layer_attn", "input_copies": len(bufs)},
+        "layer_attn_us_sum_of_stages": sum(stage_us[n] for n in names[1:]),
+        "stages": stages,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(batch, args.cpu_stride1, args.cpu_stride2)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

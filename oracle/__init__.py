@@ -70,6 +70,7 @@ class Oracle:
         self.plant = plant
         lib = ctypes.CDLL(lib_path)
         lib.daf_oracle_mutant.restype = ctypes.c_int
+        lib.daf_oracle_threads.restype = ctypes.c_int
         lib.daf_oracle_gather_rows.argtypes = [_u8p, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
         lib.daf_oracle_scatter_rows.argtypes = [_u8p, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
         lib.daf_oracle_mask_stage1.argtypes = [_i64p, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
@@ -80,6 +81,11 @@ class Oracle:
         lib.daf_oracle_masked_attention.restype = ctypes.c_int
         self.lib = lib
         self.mutant = lib.daf_oracle_mutant()
+
+    @property
+    def threads(self) -> int:
+        """OpenMP threads the oracle's loops use."""
+        return int(self.lib.daf_oracle_threads())
 
     # ---- byte-level row movement (Sec. 2 items 1 and 3) -------------------
     def gather_rows(self, src: np.ndarray, rows) -> np.ndarray:

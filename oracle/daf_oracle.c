@@ -35,6 +35,7 @@
  * show that the pins catch plausible errors. A normal build has no mutant.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -44,6 +45,9 @@
 #endif
 
 int daf_oracle_mutant(void) { return DAF_ORACLE_MUTANT; }
+
+/* Threads the OpenMP loops of this library use. */
+int daf_oracle_threads(void) { return omp_get_max_threads(); }
 
 /* Row gather, byte for byte: dst[i] = src[rows[i]].  (Sec. 2 item 1: the
  * important tokens are gathered into a condensed sequence.) */

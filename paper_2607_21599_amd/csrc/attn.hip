@@ -373,10 +373,7 @@ hipError_t launch_merge_t(const MergeLaunch &p, hipStream_t st) {
 hipError_t launch_attention(int dtype, int head_dim, AttnKind kind, const AttnLaunch &p,
                             hipStream_t st) {
   if (p.n_groups <= 0) return hipSuccess;
-  if (dtype == 0) {
-    return head_dim == 128 ? launch_attn_t<__bf16, 128>(kind, p, st)
-                           : launch_attn_t<__bf16, 64>(kind, p, st);
-  }
+  if (dtype == 0) return launch_attention_bf16(head_dim, kind, p, st);
   return head_dim == 128 ? launch_attn_t<float, 128>(kind, p, st)
                          : launch_attn_t<float, 64>(kind, p, st);
 }

@@ -1,0 +1,369 @@
+// bf16 causal GQA flash attention for both DAF attention stages (gfx950).
+//
+// Same operation and work decomposition as the fp32 kernel in attn.hip (see
+// there): query row i of a request sees keys 0 .. i + (n_keys - n_rows), a
+// workgroup of 4 waves owns 128 query rows of one head and one key split, and
+// the G heads that share a KV head form an XCD-local work group.
+//
+// bf16 data path, per 64-key tile:
+//  * K and V tiles are copied global -> LDS by the buffer unit
+//    (buffer_load_dwordx4 ... lds): no VGPR staging, no VALU address math in
+//    the loop, and rows past the end of the request read as zeros through the
+//    buffer range check. Each 1 KiB DMA instruction writes 1024/(2D) whole rows;
+//    16-byte chunks are XOR-swizzled within a row so that the two LDS read
+//    patterns below are free of bank conflicts. Two tile buffers: the DMA of
+//    tile t+1 runs while tile t is consumed, one barrier per tile.
+//  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (keys on M, query rows on N, Q in
+//    registers), so each lane owns one query row.
+//  * O^T += V^T P^T: P^T comes straight from the S^T accumulators; the V^T
+//    operand (8 consecutive keys of one feature per lane) is read from the
+//    row-major V tile with ds_read_b64_tr_b16, which transposes 16-bit data
+//    across each 16-lane group.
+//  * Online softmax in fp32, base 2, per 32-key half tile. The running max is
+//    only raised when a row's max grows by more than 2^8 (probabilities stay
+//    <= 256, exact in fp32 and bf16 range), so the O rescale is almost always
+//    skipped; the row max of a lane pair is exchanged with v_permlane32_swap.
+#include <math.h>
+
+#include "daf_internal.h"
+
+namespace daf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr int kBN = 64;                  // keys per tile
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
+constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may grow before O is rescaled
+
+template <int D>
+struct Geo {
+  static constexpr int ROWB = D * 2;         // bytes per K/V row in LDS
+  static constexpr int CH = D / 8;           // 16-byte chunks per row
+  static constexpr int TILE = kBN * ROWB;    // bytes of one K or V tile
+  static constexpr int RPI = 64 / CH;        // rows written by one 1 KiB DMA instruction
+  static constexpr int IPW = kBN / RPI / 4;  // DMA instructions per wave, per tensor and tile
+  static constexpr int DS = D / 16;          // contraction steps of S^T
+  static constexpr int DB = D / 32;          // 32-feature output blocks
+  static_assert(RPI * ROWB == 1024, "one DMA instruction writes 1 KiB");
+};
+
+// chunk swizzles (XOR, so their own inverse), both < CH
+__device__ __forceinline__ int swz_k(int r, int ch) { return r & (ch - 1); }
+__device__ __forceinline__ int swz_v(int r, int ch) { return (((r & 3) << 2) | ((r >> 2) & 3)) & (ch - 1); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// x and the same register of lane ^ 32: v_permlane32_swap on two copies of x
+// leaves {x[l % 32], x[l % 32 + 32]} in the two results. Each result element
+// is copied to a scalar before the bit cast (a bit cast of a vector element
+// expression reads the vector's first element).
+__device__ __forceinline__ void lane_pair(float x, float &a, float &b) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const unsigned r0 = r[0], r1 = r[1];
+  a = __builtin_bit_cast(float, r0);
+  b = __builtin_bit_cast(float, r1);
+}
+__device__ __forceinline__ float pair_max(float x) {
+  float a, b;
+  lane_pair(x, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  float a, b;
+  lane_pair(x, a, b);
+  return a + b;
+}
+
+__device__ __forceinline__ bf16x8 tr_pair(const unsigned char *lds_base, int off_a, int off_b) {
+  const lds_u8 *b = (const lds_u8 *)lds_base;
+  const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(b + off_a));
+  const bf16x4 c = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(b + off_b));
+  return bf16x8{a[0], a[1], a[2], a[3], c[0], c[1], c[2], c[3]};
+}
+
+// Copy one 64-key K tile and V tile global -> LDS with the buffer unit. Each
+// wave writes its IPW KiB of each tile; rows at or past n_keys read as zero.
+template <int IPW>
+__device__ __forceinline__ void dma_tile(const unsigned char *kg, const unsigned char *vg, int kb, int n_keys,
+                                         int kv_row_bytes, unsigned char *k_lds, unsigned char *v_lds, int wave,
+                                         const int (&dma_k)[IPW], const int (&dma_v)[IPW]) {
+  // The buffer->LDS builtin only exists for the GPU target; the host pass of
+  // this translation unit only needs the kernel's launch stub.
+#if defined(__HIP_DEVICE_COMPILE__)
+  const int nrec = (n_keys - kb) * kv_row_bytes;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(kg + (size_t)kb * kv_row_bytes), 0, nrec, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(vg + (size_t)kb * kv_row_bytes), 0, nrec, kRsrcWord3);
+  lds_u8 *kbase = (lds_u8 *)k_lds + wave * IPW * 1024;
+  lds_u8 *vbase = (lds_u8 *)v_lds + wave * IPW * 1024;
+#pragma unroll
+  for (int i = 0; i < IPW; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (void __attribute__((address_space(3))) *)(kbase + i * 1024), 16,
+                                             dma_k[i], 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < IPW; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (void __attribute__((address_space(3))) *)(vbase + i * 1024), 16,
+                                             dma_v[i], 0, 0, 0);
+#endif
+}
+
+// Per-wave state of one workgroup tile (lives in registers after inlining).
+template <int D>
+struct WaveState {
+  using Gm = Geo<D>;
+  bf16x8 qf[Gm::DS];       // Q rows as the B operand of S^T
+  f32x16 oacc[Gm::DB];     // O^T accumulators
+  float m_run;             // running max, scaled base-2 units, equal in both halves
+  float l_run;             // this lane's share of the row sum
+  int koff[Gm::DS];        // K tile read offsets
+  int voff[Gm::DB][2];     // V tile transposed-read offsets
+  int dma_k[Gm::IPW], dma_v[Gm::IPW];
+  const unsigned char *kg, *vg;
+  int n_keys, kv_row_bytes, limit, half, wave;
+  int wave_last_key;       // keys above this are masked for every row of the wave
+  float sl2;
+};
+
+// One 32-key half tile: scores -> online softmax -> P^T -> O^T update.
+template <int D>
+__device__ __forceinline__ void half_tile(WaveState<D> &w, const unsigned char *vs, int key0, f32x16 sacc,
+                                          bool mask) {
+  constexpr int ROWB = Geo<D>::ROWB, DB = Geo<D>::DB;
+  if (mask) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = key0 + 8 * (r >> 2) + 4 * w.half + (r & 3);
+      if (key > w.limit) sacc[r] = -INFINITY;
+    }
+  }
+  float mx = sacc[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+  const float mt = pair_max(mx) * w.sl2;
+  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(w.m_run, mt);
+    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
+    w.m_run = m_new;
+    w.l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) w.oacc[db] *= alpha;
+  }
+  const float m_use = (w.m_run == -INFINITY) ? 0.f : w.m_run;
+  float ps[4] = {0.f, 0.f, 0.f, 0.f};
+  bf16x8 pf[2];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float e = fast_exp2(__builtin_fmaf(sacc[r], w.sl2, -m_use));
+    ps[r & 3] += e;
+    pf[r >> 3][r & 7] = (__bf16)e;
+  }
+  w.l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  // O^T += V^T P^T over the 2 x 16 keys of this half tile
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const bf16x8 a = tr_pair(vs + c * 16 * ROWB, w.voff[db][0], w.voff[db][1]);
+      w.oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[c], w.oacc[db], 0, 0, 0);
+    }
+  }
+}
+
+// One 64-key tile read from buffer `ks`/`vs`; the DMA of the next tile goes to
+// `nk`/`nv`. The buffers are distinct LDS objects at each call site.
+template <int D>
+__device__ __forceinline__ void tile_step(WaveState<D> &w, const unsigned char *ks, const unsigned char *vs,
+                                          unsigned char *nk, unsigned char *nv, int kb, bool prefetch,
+                                          bool mask, bool second_half) {
+  constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS;
+  // Wait for this wave's DMA of this tile (the only vector-memory work in
+  // flight; the compiler does not count LDS DMA as a store to release), then
+  // barrier: every wave's DMA has landed and every wave is done reading the
+  // other buffer (previous tile). The fences of __syncthreads keep the
+  // compiler from moving LDS reads or the next DMA across the barrier.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt left at their maxima
+  __syncthreads();
+  if (prefetch) dma_tile<Geo<D>::IPW>(w.kg, w.vg, kb + kBN, w.n_keys, w.kv_row_bytes, nk, nv, w.wave, w.dma_k, w.dma_v);
+  if (kb > w.wave_last_key) return;  // the whole tile is masked for this wave
+  f32x16 sacc[2];
+#pragma unroll
+  for (int b2 = 0; b2 < 2; ++b2) {
+    sacc[b2] = f32x16{};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
+      sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, w.qf[ds], sacc[b2], 0, 0, 0);
+    }
+  }
+  half_tile<D>(w, vs, kb, sacc[0], mask);
+  if (second_half) half_tile<D>(w, vs + 32 * ROWB, kb + 32, sacc[1], mask);
+}
+
+template <int D, int KIND>
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLaunch p) {
+  using Gm = Geo<D>;
+  constexpr int ROWB = Gm::ROWB, CH = Gm::CH, TILE = Gm::TILE, IPW = Gm::IPW, DS = Gm::DS, DB = Gm::DB;
+  constexpr int RPI = Gm::RPI;
+  // separate objects per stage and tensor: lets the compiler see that the DMA
+  // into one buffer does not alias reads of another
+  __shared__ __attribute__((aligned(1024))) unsigned char k_lds0[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
+
+  // ---- which work: XCD-aware deal of work groups ----------------------------
+  const int G = p.group;
+  const int xcd = blockIdx.x % kXcds;
+  const int slot = blockIdx.x / kXcds;
+  const int gamma = (slot / G) * kXcds + xcd;
+  const int hl = slot % G;
+  if (gamma >= p.n_groups) return;
+  int ei = 0;
+  while (ei + 1 < p.n_entries && p.e[ei + 1].group0 <= gamma) ++ei;
+  const AttnEntry &E = p.e[ei];
+  int gl = gamma - E.group0;
+  const int g = gl % p.hkv;
+  gl /= p.hkv;
+  const int s = gl % E.n_splits;
+  gl /= E.n_splits;
+  const int mb = E.mb_hi - gl;
+  const int h = g * G + hl;
+
+  const int n_rows = E.n_rows;
+  const int n_keys = E.n_keys;
+  const int offset = n_keys - n_rows;
+  const int row0 = mb * kAttnBM;
+  const int row_last = min(row0 + kAttnBM, n_rows) - 1;
+  const int k_begin = s * E.split_keys;
+  const int k_end = min(min(k_begin + E.split_keys, n_keys), row_last + offset + 1);
+  const int n_tiles = k_end > k_begin ? (k_end - k_begin + kBN - 1) / kBN : 0;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int l32 = lane & 31;
+  const int half = lane >> 5;
+  const int wrow0 = row0 + wave * 32;
+  const int my_row = wrow0 + l32;
+  const int wave_last_key = wrow0 + 31 + offset;  // keys above this are masked for the whole wave
+
+  WaveState<D> w;
+  w.kg = static_cast<const unsigned char *>(E.k);
+  w.vg = static_cast<const unsigned char *>(E.v);
+  w.n_keys = n_keys;
+  w.kv_row_bytes = p.hkv * D * 2;
+  w.limit = my_row + offset;
+  w.wave_last_key = wave_last_key;
+  w.half = half;
+  w.wave = wave;
+  w.sl2 = p.scale_log2;
+  w.m_run = -INFINITY;
+  w.l_run = 0.f;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) w.oacc[db] = f32x16{};
+  {
+    const __bf16 *qp = static_cast<const __bf16 *>(E.q) + ((size_t)my_row * p.hq + h) * D + 8 * half;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+      w.qf[ds] = my_row < n_rows ? *reinterpret_cast<const bf16x8 *>(qp + 16 * ds) : bf16x8{};
+  }
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int r = (wave * IPW + i) * RPI + lane / CH;
+    const int pc = lane % CH;
+    w.dma_k[i] = r * w.kv_row_bytes + g * D * 2 + ((pc ^ swz_k(r, CH)) << 4);
+    w.dma_v[i] = r * w.kv_row_bytes + g * D * 2 + ((pc ^ swz_v(r, CH)) << 4);
+  }
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) w.koff[ds] = l32 * ROWB + (((2 * ds + half) ^ swz_k(l32, CH)) << 4);
+  {
+    const int grp = lane >> 4, j = lane & 15;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int key = 8 * b + 4 * (grp >> 1) + (j >> 2);
+      const int sw = swz_v(key, CH);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int lc = 4 * db + 2 * (grp & 1) + ((j & 3) >> 1);
+        w.voff[db][b] = key * ROWB + ((lc ^ sw) << 4) + 8 * (j & 1);
+      }
+    }
+  }
+
+  if (n_tiles > 0) dma_tile<IPW>(w.kg, w.vg, k_begin, n_keys, w.kv_row_bytes, k_lds0, v_lds0, wave, w.dma_k, w.dma_v);
+  for (int t = 0; t < n_tiles; t += 2) {
+    // even tiles live in buffer 0, odd tiles in buffer 1
+    int kb = k_begin + t * kBN;
+    tile_step<D>(w, k_lds0, v_lds0, k_lds1, v_lds1, kb, t + 1 < n_tiles, (kb + kBN - 1) > (wrow0 + offset),
+                 kb + 32 <= wave_last_key);
+    if (t + 1 < n_tiles) {
+      kb += kBN;
+      tile_step<D>(w, k_lds1, v_lds1, k_lds0, v_lds0, kb, t + 2 < n_tiles, (kb + kBN - 1) > (wrow0 + offset),
+                   kb + 32 <= wave_last_key);
+    }
+  }
+
+  // ---- epilogue ---------------------------------------------------------------
+  const float l_tot = pair_sum(w.l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse_nat = l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+  if (my_row >= n_rows) return;
+  if (E.n_splits == 1 && E.o != nullptr) {
+    __bf16 *op = static_cast<__bf16 *>(E.o) + ((size_t)my_row * p.hq + h) * D + 4 * half;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        bf16x4 v;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = (__bf16)(w.oacc[db][4 * q4 + t] * inv);
+        *reinterpret_cast<bf16x4 *>(op + db * 32 + 8 * q4) = v;
+      }
+    }
+    if (E.lse != nullptr && half == 0) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
+  } else {
+    const size_t prow = (size_t)my_row * E.n_splits + s;
+    float *op = E.part_o + (prow * p.hq + h) * D + 4 * half;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        f32x4 v;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = w.oacc[db][4 * q4 + t] * inv;
+        *reinterpret_cast<f32x4 *>(op + db * 32 + 8 * q4) = v;
+      }
+    }
+    if (half == 0) E.part_lse[prow * p.hq + h] = lse_nat;
+  }
+}
+
+template <int D>
+hipError_t launch_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
+  const int slots = p.group * ((p.n_groups + kXcds - 1) / kXcds);
+  const dim3 grid(kXcds * slots), block(kAttnThreads);
+  switch (kind) {
+    case AttnKind::kSelf: attn_bf16_kernel<D, 0><<<grid, block, 0, st>>>(p); break;
+    case AttnKind::kQdoc: attn_bf16_kernel<D, 1><<<grid, block, 0, st>>>(p); break;
+    default: attn_bf16_kernel<D, 2><<<grid, block, 0, st>>>(p); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention_bf16(int head_dim, AttnKind kind, const AttnLaunch &p, hipStream_t st) {
+  if (p.n_groups <= 0) return hipSuccess;
+  return head_dim == 128 ? launch_t<128>(kind, p, st) : launch_t<64>(kind, p, st);
+}
+
+}  // namespace daf

@@ -93,6 +93,8 @@ struct ScatterPair {
 enum class AttnKind { kSelf = 0, kQdoc = 1, kLayer = 2 };
 hipError_t launch_attention(int dtype, int head_dim, AttnKind kind,
                             const AttnLaunch &p, hipStream_t s);
+hipError_t launch_attention_bf16(int head_dim, AttnKind kind, const AttnLaunch &p,
+                                 hipStream_t s);
 hipError_t launch_merge(int dtype, int head_dim, const MergeLaunch &p,
                         hipStream_t s);
 hipError_t launch_gather(const RowLaunch &p, int64_t src_base_unused,
