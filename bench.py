@@ -101,6 +101,9 @@ def main():
     ap.add_argument("--cpu-stride1", type=int, default=4)
     ap.add_argument("--cpu-stride2", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="before timing, run one plain device copy of this many MiB (a known-size "
+                         "kernel that calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only (the DAF layer attention is measured on a "
@@ -128,6 +131,14 @@ def main():
         bufs[j].gather_hidden(gath[j])
         bufs[j].layer()
 
+    if args.calib_copy_mb > 0:
+        n = args.calib_copy_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
