@@ -107,6 +107,19 @@ daf_status_t parse_batch(const daf_batch_t *b, Batch &out) {
   return DAF_OK;
 }
 
+// The attention kernels address one request's K/V rows through buffer
+// descriptors with 32-bit byte offsets.
+daf_status_t check_kv_extent(const Cfg &c, const Batch &b) {
+  const int64_t row = (int64_t)c.hkv * c.d * c.elem;
+  for (size_t i = 0; i < b.r.size(); ++i) {
+    const int64_t t = (int64_t)b.r[i].L_d + b.r[i].L_q;
+    if (t * row > INT32_MAX)
+      return fail(DAF_ERR_UNSUPPORTED, "request %zu: %lld K/V bytes exceed 2 GiB per request", i,
+                  (long long)(t * row));
+  }
+  return DAF_OK;
+}
+
 daf_status_t need_ptr(const void *p, const char *name) {
   if (!p) return fail(DAF_ERR_INVALID_ARG, "%s is NULL", name);
   if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
@@ -234,19 +247,28 @@ daf_status_t run_entries(const Cfg &c, AttnKind kind, std::vector<AttnEntry> &en
 }
 
 void add_self_entries(const Cfg &c, const Batch &b, const void *q_imp, const void *k_imp,
-                      const void *v_imp, void *o_imp, float *lse_imp, std::vector<AttnEntry> &out) {
+                      const void *v_imp, void *o_imp, float *lse_imp, std::vector<AttnEntry> &out,
+                      void *hidden = nullptr, const int32_t *idx = nullptr) {
   // heaviest requests first: their top query blocks carry the most work
   std::vector<int> order;
   for (int i = 0; i < (int)b.r.size(); ++i)
     if (b.r[i].n > 0) order.push_back(i);
   std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return b.r[x].n > b.r[y].n; });
-  for (int i : order) out.push_back(self_entry(c, b.r[i], b.total_imp, q_imp, k_imp, v_imp, o_imp, lse_imp));
+  for (int i : order) {
+    AttnEntry e = self_entry(c, b.r[i], b.total_imp, q_imp, k_imp, v_imp, o_imp, lse_imp);
+    if (hidden) {
+      e.o2 = hidden;
+      e.o2_idx = idx + b.r[i].imp0;
+      e.o2_row0 = b.r[i].tok0;
+    }
+    out.push_back(e);
+  }
 }
 
 daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const void *k_cache,
                           const void *v_cache, void *workspace, size_t ws_bytes,
                           std::vector<AttnEntry> &out, std::vector<MergeEntry> &merge, void *o_q,
-                          float *lse_q) {
+                          float *lse_q, void *hidden = nullptr) {
   const std::vector<Split> sp = plan_splits(c, b);
   const WsLayout w = ws_layout(c, b, sp);
   if (w.part_rows == 0) return DAF_OK;
@@ -270,6 +292,10 @@ daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const v
     m.lse_stride = (int32_t)b.total_q;
     m.n_rows = q.L_q;
     m.n_splits = sp[i].n_splits;
+    if (hidden) {
+      m.o2 = hidden;
+      m.o2_row0 = q.tok0 + q.L_d;
+    }
     merge.push_back(m);
     prow += (int64_t)q.L_q * sp[i].n_splits;
   }
@@ -428,6 +454,7 @@ daf_status_t daf_imp_self_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *bat
     Batch b;
     CHECK(parse_cfg(cfg, c));
     CHECK(parse_batch(batch, b));
+    CHECK(check_kv_extent(c, b));
     if (b.total_imp == 0) return ok();
     CHECK(need_ptr(q_imp, "q_imp"));
     CHECK(need_ptr(k_imp, "k_imp"));
@@ -467,6 +494,7 @@ daf_status_t daf_qdoc_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, 
     Batch b;
     CHECK(parse_cfg(cfg, c));
     CHECK(parse_batch(batch, b));
+    CHECK(check_kv_extent(c, b));
     if (b.total_q == 0) return ok();
     CHECK(need_ptr(q_q, "q_q"));
     CHECK(need_ptr(k_cache, "k_cache"));
@@ -511,6 +539,7 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
     Batch b;
     CHECK(parse_cfg(cfg, c));
     CHECK(parse_batch(batch, b));
+    CHECK(check_kv_extent(c, b));
     const uint32_t both = DAF_FUSE_KV | DAF_FUSE_HIDDEN;
     if (b.total_imp == 0 && b.total_q == 0) return ok();
     CHECK(check_fuse_ptrs(b, both, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, o_imp, o_q, hidden));
@@ -519,18 +548,22 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
     if (lse_imp) CHECK(need_ptr(lse_imp, "lse_imp"));
     if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
     // plan (and check the workspace) before enqueueing anything
-    std::vector<AttnEntry> entries;
+    std::vector<AttnEntry> self, qdoc;
     std::vector<MergeEntry> merge;
-    add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, entries);
-    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, entries, merge, o_q, lse_q));
-    // hybrid KV first (stage 2 reads it), then both attention stages in one
-    // grid, the split merge, and the fusion into the hidden states
+    // the epilogues also fuse the outputs into the hidden states: stage-1 row i
+    // of request b goes to hidden[tok_b + idx[i]], question row j (written by
+    // the merge) to hidden[tok_b + L_d,b + j]
+    add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, self, hidden, idx);
+    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, merge, o_q, lse_q, hidden));
+    // hybrid KV first (stage 2 reads it), then the attention stages and the
+    // split merge, whose epilogues also fuse the outputs into the hidden states
     CHECK(fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr, nullptr,
                     nullptr, stream));
-    CHECK(run_entries(c, AttnKind::kLayer, entries, stream));
+    // stage 2 then stage 1 as two grids: one grid holding both runs slower
+    // (stage 2's cache stream evicts the stage-1 K/V each XCD's L2 holds)
+    CHECK(run_entries(c, AttnKind::kQdoc, qdoc, stream));
     CHECK(run_merge(c, merge, stream));
-    CHECK(fuse_impl(c, b, DAF_FUSE_HIDDEN, idx, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                    o_imp, o_q, hidden, stream));
+    CHECK(run_entries(c, AttnKind::kSelf, self, stream));
     return ok();
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");

@@ -5,8 +5,8 @@
 // same operation: query row i of a request sees keys 0 .. i + (n_keys -
 // n_rows). Stage 1 has n_keys == n_rows (plain causal over the condensed
 // sequence); stage 2 has n_rows = L_q question rows over n_keys = L_d + L_q
-// cache rows. A launch carries a table of entries (requests of either stage),
-// so one grid can run stage 1 and stage 2 side by side.
+// cache rows. A launch carries a table of entries (requests, possibly ragged,
+// each a range of query blocks with its own key split).
 //
 // Work decomposition. A workgroup (4 waves) owns 128 query rows of one query
 // head and one key split. The G = Hq/Hkv workgroups that read the same K/V
@@ -286,6 +286,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
   if (my_row >= n_rows) return;
   if (E.n_splits == 1 && E.o != nullptr) {
     T *op = static_cast<T *>(E.o) + ((size_t)my_row * p.hq + h) * D + 4 * half;
+    T *op2 = nullptr;
+    if (E.o2 != nullptr) {
+      const int64_t r2 = E.o2_row0 + (E.o2_idx ? E.o2_idx[my_row] : my_row);
+      op2 = static_cast<T *>(E.o2) + ((size_t)r2 * p.hq + h) * D + 4 * half;
+    }
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -294,6 +299,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
 #pragma unroll
         for (int t = 0; t < 4; ++t) w[t] = (T)(oacc[db][4 * q4 + t] * inv);
         *reinterpret_cast<V4 *>(op + db * 32 + 8 * q4) = w;
+        if (op2) *reinterpret_cast<V4 *>(op2 + db * 32 + 8 * q4) = w;
       }
     }
     if (E.lse != nullptr && half == 0) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
@@ -314,11 +320,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
   }
 }
 
-// Log-sum-exp merge of the key splits: one wave per (query row, head).
+// Log-sum-exp merge of the key splits. D/4 threads per (query row, head), each
+// owning 4 features: m = max_s lse_s, w_s = exp(lse_s - m), O = sum_s w_s O_s /
+// sum_s w_s, lse = m + log sum_s w_s. Split partials are read with 16-byte
+// loads, several splits in flight per thread.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
-  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  constexpr int TPI = D / 4;             // threads per (row, head) item
+  constexpr int IPB = 256 / TPI;         // items per block
+  const int item = blockIdx.x * IPB + threadIdx.x / TPI;
+  const int t = threadIdx.x % TPI;
   const int row = item / p.hq, h = item % p.hq;
   if (row >= p.total_rows) return;
   int ei = 0;
@@ -327,26 +338,51 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
   const int r = row - E.row0;
   const int S = E.n_splits;
   const size_t prow0 = (size_t)r * S;
-  float m = -INFINITY;
-  for (int s = 0; s < S; ++s) m = fmaxf(m, E.part_lse[(prow0 + s) * p.hq + h]);
-  constexpr int PER = D / 64;  // features per lane
-  float acc[PER];
+  const float *lse = E.part_lse + prow0 * p.hq + h;
+  const float *src = E.part_o + (prow0 * p.hq + h) * D + 4 * t;
+  const size_t split_stride = (size_t)p.hq * D;
+  // the loads of up to U splits go out before any of them is used
+  constexpr int U = 16;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, wsum = 0.f;
+  for (int s0 = 0; s0 < S; s0 += U) {
+    float ls[U];
+    f32x4 po[U];
 #pragma unroll
-  for (int j = 0; j < PER; ++j) acc[j] = 0.f;
-  float wsum = 0.f;
-  for (int s = 0; s < S; ++s) {
-    const float ls = E.part_lse[(prow0 + s) * p.hq + h];
-    const float w = (ls == -INFINITY) ? 0.f : __expf(ls - m);
-    wsum += w;
-    const float *src = E.part_o + ((prow0 + s) * p.hq + h) * D + lane * PER;
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < S) {
+        ls[u] = lse[(size_t)(s0 + u) * p.hq];
+        po[u] = *reinterpret_cast<const f32x4 *>(src + (s0 + u) * split_stride);
+      } else {
+        ls[u] = -INFINITY;
+        po[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    float mc = m;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) acc[j] += w * src[j];
+    for (int u = 0; u < U; ++u) mc = fmaxf(mc, ls[u]);
+    // rescale what earlier chunks accumulated to the new max
+    const float a = (m == -INFINITY) ? 0.f : __expf(m - mc);
+    acc *= a;
+    wsum *= a;
+    m = mc;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float w = (ls[u] == -INFINITY) ? 0.f : __expf(ls[u] - m);
+      wsum += w;
+      acc += w * po[u];
+    }
   }
   const float inv = 1.f / wsum;
-  T *dst = static_cast<T *>(E.o) + ((size_t)r * p.hq + h) * D + lane * PER;
+  T *dst = static_cast<T *>(E.o) + ((size_t)r * p.hq + h) * D + 4 * t;
+  typename Vec<T>::v4 o;
 #pragma unroll
-  for (int j = 0; j < PER; ++j) dst[j] = (T)(acc[j] * inv);
-  if (E.lse != nullptr && lane == 0) E.lse[(size_t)h * E.lse_stride + r] = m + __logf(wsum);
+  for (int j = 0; j < 4; ++j) o[j] = (T)(acc[j] * inv);
+  *reinterpret_cast<typename Vec<T>::v4 *>(dst) = o;
+  if (E.o2 != nullptr)
+    *reinterpret_cast<typename Vec<T>::v4 *>(static_cast<T *>(E.o2) +
+                                             ((size_t)(E.o2_row0 + r) * p.hq + h) * D + 4 * t) = o;
+  if (E.lse != nullptr && t == 0) E.lse[(size_t)h * E.lse_stride + r] = m + __logf(wsum);
 }
 
 template <typename T, int D>
@@ -355,8 +391,7 @@ hipError_t launch_attn_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
   const dim3 grid(kXcds * slots), block(kAttnThreads);
   switch (kind) {
     case AttnKind::kSelf: attn_fwd_kernel<T, D, 0><<<grid, block, 0, st>>>(p); break;
-    case AttnKind::kQdoc: attn_fwd_kernel<T, D, 1><<<grid, block, 0, st>>>(p); break;
-    default: attn_fwd_kernel<T, D, 2><<<grid, block, 0, st>>>(p); break;
+    default: attn_fwd_kernel<T, D, 1><<<grid, block, 0, st>>>(p); break;
   }
   return hipGetLastError();
 }
@@ -364,7 +399,8 @@ hipError_t launch_attn_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
 template <typename T, int D>
 hipError_t launch_merge_t(const MergeLaunch &p, hipStream_t st) {
   const int items = p.total_rows * p.hq;
-  lse_merge_kernel<T, D><<<dim3((items + 3) / 4), dim3(256), 0, st>>>(p);
+  constexpr int IPB = 256 / (D / 4);
+  lse_merge_kernel<T, D><<<dim3((items + IPB - 1) / IPB), dim3(256), 0, st>>>(p);
   return hipGetLastError();
 }
 

@@ -130,36 +130,14 @@ struct WaveState {
   const unsigned char *kg, *vg;
   int n_keys, kv_row_bytes, limit, half, wave;
   int wave_last_key;       // keys above this are masked for every row of the wave
+  int wave_first_limit;    // keys up to this are visible to every row of the wave
   float sl2;
 };
 
-// One 32-key half tile: scores -> online softmax -> P^T -> O^T update.
+// P^T operands (bf16) of one 32-key half and the running row-sum update.
 template <int D>
-__device__ __forceinline__ void half_tile(WaveState<D> &w, const unsigned char *vs, int key0, f32x16 sacc,
-                                          bool mask) {
-  constexpr int ROWB = Geo<D>::ROWB, DB = Geo<D>::DB;
-  if (mask) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = key0 + 8 * (r >> 2) + 4 * w.half + (r & 3);
-      if (key > w.limit) sacc[r] = -INFINITY;
-    }
-  }
-  float mx = sacc[0];
-#pragma unroll
-  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-  const float mt = pair_max(mx) * w.sl2;
-  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
-    const float m_new = fmaxf(w.m_run, mt);
-    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
-    w.m_run = m_new;
-    w.l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) w.oacc[db] *= alpha;
-  }
-  const float m_use = (w.m_run == -INFINITY) ? 0.f : w.m_run;
+__device__ __forceinline__ void softmax_half(WaveState<D> &w, const f32x16 &sacc, float m_use, bf16x8 (&pf)[2]) {
   float ps[4] = {0.f, 0.f, 0.f, 0.f};
-  bf16x8 pf[2];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float e = fast_exp2(__builtin_fmaf(sacc[r], w.sl2, -m_use));
@@ -167,7 +145,12 @@ __device__ __forceinline__ void half_tile(WaveState<D> &w, const unsigned char *
     pf[r >> 3][r & 7] = (__bf16)e;
   }
   w.l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-  // O^T += V^T P^T over the 2 x 16 keys of this half tile
+}
+
+// O^T += V^T P^T over the 2 x 16 keys of one half tile.
+template <int D>
+__device__ __forceinline__ void pv_half(WaveState<D> &w, const unsigned char *vs, const bf16x8 (&pf)[2]) {
+  constexpr int ROWB = Geo<D>::ROWB, DB = Geo<D>::DB;
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
 #pragma unroll
@@ -178,13 +161,65 @@ __device__ __forceinline__ void half_tile(WaveState<D> &w, const unsigned char *
   }
 }
 
+// One 64-key tile: S^T = K Q^T, online softmax (one max per tile), O^T update.
+// MASK selects the diagonal-tile variant (causal mask, possibly a fully masked
+// second half); full tiles run straight-line code so the scheduler can overlap
+// the P.V MFMAs of one half with the softmax of the other.
+template <int D, bool MASK>
+__device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *ks, const unsigned char *vs, int kb) {
+  constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS, DB = Geo<D>::DB;
+  const bool second = !MASK || (kb + 32 <= w.wave_last_key);
+  f32x16 sacc[2];
+#pragma unroll
+  for (int b2 = 0; b2 < 2; ++b2) {
+    if (MASK && b2 == 1 && !second) {
+      sacc[1] = f32x16{};
+      continue;
+    }
+    bf16x8 kf[DS];
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) kf[ds] = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
+    sacc[b2] = f32x16{};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ds], w.qf[ds], sacc[b2], 0, 0, 0);
+  }
+  if (MASK) {
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + 32 * b2 + 8 * (r >> 2) + 4 * w.half + (r & 3);
+        if (key > w.limit) sacc[b2][r] = -INFINITY;
+      }
+    }
+  }
+  float mx = fmaxf(sacc[0][0], sacc[1][0]);
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sacc[0][r], sacc[1][r]));
+  const float mt = pair_max(mx) * w.sl2;
+  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(w.m_run, mt);
+    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
+    w.m_run = m_new;
+    w.l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) w.oacc[db] *= alpha;
+  }
+  const float m_use = (w.m_run == -INFINITY) ? 0.f : w.m_run;
+  bf16x8 pf0[2], pf1[2];
+  softmax_half<D>(w, sacc[0], m_use, pf0);
+  pv_half<D>(w, vs, pf0);
+  if (second) {
+    softmax_half<D>(w, sacc[1], m_use, pf1);
+    pv_half<D>(w, vs + 32 * ROWB, pf1);
+  }
+}
+
 // One 64-key tile read from buffer `ks`/`vs`; the DMA of the next tile goes to
 // `nk`/`nv`. The buffers are distinct LDS objects at each call site.
 template <int D>
 __device__ __forceinline__ void tile_step(WaveState<D> &w, const unsigned char *ks, const unsigned char *vs,
-                                          unsigned char *nk, unsigned char *nv, int kb, bool prefetch,
-                                          bool mask, bool second_half) {
-  constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS;
+                                          unsigned char *nk, unsigned char *nv, int kb, bool prefetch) {
   // Wait for this wave's DMA of this tile (the only vector-memory work in
   // flight; the compiler does not count LDS DMA as a store to release), then
   // barrier: every wave's DMA has landed and every wave is done reading the
@@ -193,19 +228,9 @@ __device__ __forceinline__ void tile_step(WaveState<D> &w, const unsigned char *
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt left at their maxima
   __syncthreads();
   if (prefetch) dma_tile<Geo<D>::IPW>(w.kg, w.vg, kb + kBN, w.n_keys, w.kv_row_bytes, nk, nv, w.wave, w.dma_k, w.dma_v);
-  if (kb > w.wave_last_key) return;  // the whole tile is masked for this wave
-  f32x16 sacc[2];
-#pragma unroll
-  for (int b2 = 0; b2 < 2; ++b2) {
-    sacc[b2] = f32x16{};
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
-      sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, w.qf[ds], sacc[b2], 0, 0, 0);
-    }
-  }
-  half_tile<D>(w, vs, kb, sacc[0], mask);
-  if (second_half) half_tile<D>(w, vs + 32 * ROWB, kb + 32, sacc[1], mask);
+  if (kb > w.wave_last_key) return;               // the whole tile is masked for this wave
+  if (kb + kBN - 1 > w.wave_first_limit) tile_math<D, true>(w, ks, vs, kb);
+  else tile_math<D, false>(w, ks, vs, kb);
 }
 
 template <int D, int KIND>
@@ -220,22 +245,35 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
   __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
 
-  // ---- which work: XCD-aware deal of work groups ----------------------------
+  // ---- which work -----------------------------------------------------------
+  // A work group is the G heads that share one KV head, for one entry, query
+  // block and key split. When Hkv divides the 8 XCDs, each XCD serves one KV
+  // head (8/Hkv XCDs per head), so every L2 holds the K/V of a single head;
+  // otherwise work groups are dealt to the XCDs round-robin. Within an XCD,
+  // work groups run heaviest first, and the G heads of a work group are
+  // consecutive workgroups of that XCD.
   const int G = p.group;
   const int xcd = blockIdx.x % kXcds;
   const int slot = blockIdx.x / kXcds;
-  const int gamma = (slot / G) * kXcds + xcd;
   const int hl = slot % G;
-  if (gamma >= p.n_groups) return;
+  int g, lam;  // KV head, index of the work group among that head's work groups
+  if (kXcds % p.hkv == 0) {
+    const int xph = kXcds / p.hkv;
+    g = xcd / xph;
+    lam = (slot / G) * xph + xcd % xph;
+    if (lam * p.hkv >= p.n_groups) return;
+  } else {
+    const int gamma = (slot / G) * kXcds + xcd;
+    if (gamma >= p.n_groups) return;
+    g = gamma % p.hkv;
+    lam = gamma / p.hkv;
+  }
   int ei = 0;
-  while (ei + 1 < p.n_entries && p.e[ei + 1].group0 <= gamma) ++ei;
+  while (ei + 1 < p.n_entries && p.e[ei + 1].group0 <= lam * p.hkv) ++ei;
   const AttnEntry &E = p.e[ei];
-  int gl = gamma - E.group0;
-  const int g = gl % p.hkv;
-  gl /= p.hkv;
-  const int s = gl % E.n_splits;
-  gl /= E.n_splits;
-  const int mb = E.mb_hi - gl;
+  const int ll = lam - E.group0 / p.hkv;
+  const int s = ll % E.n_splits;
+  const int mb = E.mb_hi - ll / E.n_splits;
   const int h = g * G + hl;
 
   const int n_rows = E.n_rows;
@@ -263,6 +301,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   w.kv_row_bytes = p.hkv * D * 2;
   w.limit = my_row + offset;
   w.wave_last_key = wave_last_key;
+  w.wave_first_limit = wrow0 + offset;
   w.half = half;
   w.wave = wave;
   w.sl2 = p.scale_log2;
@@ -303,12 +342,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   for (int t = 0; t < n_tiles; t += 2) {
     // even tiles live in buffer 0, odd tiles in buffer 1
     int kb = k_begin + t * kBN;
-    tile_step<D>(w, k_lds0, v_lds0, k_lds1, v_lds1, kb, t + 1 < n_tiles, (kb + kBN - 1) > (wrow0 + offset),
-                 kb + 32 <= wave_last_key);
+    tile_step<D>(w, k_lds0, v_lds0, k_lds1, v_lds1, kb, t + 1 < n_tiles);
     if (t + 1 < n_tiles) {
       kb += kBN;
-      tile_step<D>(w, k_lds1, v_lds1, k_lds0, v_lds0, kb, t + 2 < n_tiles, (kb + kBN - 1) > (wrow0 + offset),
-                   kb + 32 <= wave_last_key);
+      tile_step<D>(w, k_lds1, v_lds1, k_lds0, v_lds0, kb, t + 2 < n_tiles);
     }
   }
 
@@ -319,6 +356,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   if (my_row >= n_rows) return;
   if (E.n_splits == 1 && E.o != nullptr) {
     __bf16 *op = static_cast<__bf16 *>(E.o) + ((size_t)my_row * p.hq + h) * D + 4 * half;
+    __bf16 *op2 = nullptr;
+    if (E.o2 != nullptr) {
+      const int64_t r2 = E.o2_row0 + (E.o2_idx ? E.o2_idx[my_row] : my_row);
+      op2 = static_cast<__bf16 *>(E.o2) + ((size_t)r2 * p.hq + h) * D + 4 * half;
+    }
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -327,6 +369,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
 #pragma unroll
         for (int t = 0; t < 4; ++t) v[t] = (__bf16)(w.oacc[db][4 * q4 + t] * inv);
         *reinterpret_cast<bf16x4 *>(op + db * 32 + 8 * q4) = v;
+        if (op2) *reinterpret_cast<bf16x4 *>(op2 + db * 32 + 8 * q4) = v;
       }
     }
     if (E.lse != nullptr && half == 0) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
@@ -349,12 +392,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
 
 template <int D>
 hipError_t launch_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
-  const int slots = p.group * ((p.n_groups + kXcds - 1) / kXcds);
+  // slots per XCD: work groups per XCD times the G heads of a work group
+  int per_xcd;
+  if (kXcds % p.hkv == 0) {
+    const int xph = kXcds / p.hkv, per_head = p.n_groups / p.hkv;
+    per_xcd = (per_head + xph - 1) / xph;
+  } else {
+    per_xcd = (p.n_groups + kXcds - 1) / kXcds;
+  }
+  const int slots = p.group * per_xcd;
   const dim3 grid(kXcds * slots), block(kAttnThreads);
   switch (kind) {
     case AttnKind::kSelf: attn_bf16_kernel<D, 0><<<grid, block, 0, st>>>(p); break;
-    case AttnKind::kQdoc: attn_bf16_kernel<D, 1><<<grid, block, 0, st>>>(p); break;
-    default: attn_bf16_kernel<D, 2><<<grid, block, 0, st>>>(p); break;
+    default: attn_bf16_kernel<D, 1><<<grid, block, 0, st>>>(p); break;
   }
   return hipGetLastError();
 }

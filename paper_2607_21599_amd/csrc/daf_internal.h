@@ -10,7 +10,7 @@ namespace daf {
 constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round-robin
 constexpr int kAttnThreads = 256; // 4 waves, 32 query rows each
 constexpr int kAttnBM = 128;      // query rows per attention workgroup
-constexpr int kMaxEntries = 16;   // work-table entries per attention launch
+constexpr int kMaxEntries = 32;   // work-table entries per attention launch (kernel argument < 4 KiB)
 constexpr int kMaxRowReqs = 32;   // requests per row-movement launch
 constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident attention workgroups
 
@@ -35,8 +35,15 @@ struct AttnEntry {
   int32_t n_splits;   // key splits (1 = direct mode)
   int32_t split_keys; // keys per split, a multiple of the key tile
   int32_t group0;     // first work group (G query heads sharing a KV head)
+  // optional second destination of each final output row (the state fusion
+  // into the hidden states): row i goes to o2 row o2_row0 + (o2_idx ? o2_idx[i] : i)
+  void *o2;
+  const int32_t *o2_idx;
+  int64_t o2_row0;
 };
 
+struct AttnLaunch;
+static_assert(sizeof(AttnEntry) * kMaxEntries + 64 < 4096, "attention launch table must fit 4 KiB of kernel arguments");
 struct AttnLaunch {
   int32_t hq, hkv, group;  // group = Hq / Hkv
   int32_t n_entries;
@@ -55,6 +62,8 @@ struct MergeEntry {
   int32_t n_rows;
   int32_t n_splits;
   int32_t row0;   // first global (row, head) item / Hq of this entry
+  void *o2;       // optional second destination, row r -> o2 row o2_row0 + r
+  int64_t o2_row0;
 };
 
 struct MergeLaunch {
@@ -90,7 +99,8 @@ struct ScatterPair {
 };
 
 // Kernel launchers (defined in attn.hip / rows.hip). Return the launch error.
-enum class AttnKind { kSelf = 0, kQdoc = 1, kLayer = 2 };
+// kernel names differ per stage so that profiles tell the stages apart
+enum class AttnKind { kSelf = 0, kQdoc = 1 };
 hipError_t launch_attention(int dtype, int head_dim, AttnKind kind,
                             const AttnLaunch &p, hipStream_t s);
 hipError_t launch_attention_bf16(int head_dim, AttnKind kind, const AttnLaunch &p,

@@ -86,6 +86,27 @@ def test_gather_bit_exact(name):
     assert np.array_equal(_raw(kdst), kexp)
 
 
+def test_gather_wide_rows():
+    """Rows wider than 8 KiB (moved in column chunks) and ragged requests."""
+    import paper_2607_21599_amd as daf
+    from paper_2607_21599_amd.tensors import to_device
+    rng = np.random.Generator(np.random.PCG64(9))
+    cu_doc, cu_q, cu_imp = [0, 700, 1000, 1900], [0, 3, 3, 10], [0, 41, 41, 300]
+    row_bytes = 20000
+    total_tok = cu_doc[-1] + cu_q[-1]
+    src = rng.integers(0, 256, size=(total_tok, row_bytes), dtype=np.uint8)
+    idx = np.concatenate([np.sort(rng.choice(cu_doc[b + 1] - cu_doc[b], cu_imp[b + 1] - cu_imp[b],
+                                             replace=False)) for b in range(3)]).astype(np.int32)
+    b = daf.Batch(cu_doc, cu_q, cu_imp)
+    s_dev = torch.from_numpy(src).cuda()
+    dst = torch.zeros((cu_imp[-1], row_bytes), dtype=torch.uint8, device="cuda")
+    daf.daf_gather_important(b, daf.DAF_SRC_TOKENS, s_dev, row_bytes, to_device(idx), dst)
+    torch.cuda.synchronize()
+    tok0 = [cu_doc[k] + cu_q[k] for k in range(3)]
+    rows = np.concatenate([tok0[k] + idx[cu_imp[k]:cu_imp[k + 1]] for k in range(3)])
+    assert np.array_equal(dst.cpu().numpy(), orc_mod.get().gather_rows(src, rows))
+
+
 @pytest.mark.parametrize("name", ["tiny_f32_1k", "qwen7b_6k", "qwen7b_batch8"])
 def test_fuse_bit_exact(name):
     """KV mode builds the hybrid cache; hidden mode scatters stage outputs
