@@ -151,14 +151,16 @@ __device__ __forceinline__ void softmax_half(WaveState<D> &w, const f32x16 &sacc
 template <int D>
 __device__ __forceinline__ void pv_half(WaveState<D> &w, const unsigned char *vs, const bf16x8 (&pf)[2]) {
   constexpr int ROWB = Geo<D>::ROWB, DB = Geo<D>::DB;
+  // all transposed V reads of the half tile before its MFMAs
+  bf16x8 a[2][DB];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < 2; ++c)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const bf16x8 a = tr_pair(vs + c * 16 * ROWB, w.voff[db][0], w.voff[db][1]);
-      w.oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[c], w.oacc[db], 0, 0, 0);
-    }
-  }
+    for (int db = 0; db < DB; ++db) a[c][db] = tr_pair(vs + c * 16 * ROWB, w.voff[db][0], w.voff[db][1]);
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) w.oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[c][db], pf[c], w.oacc[db], 0, 0, 0);
 }
 
 // One 64-key tile: S^T = K Q^T, online softmax (one max per tile), O^T update.
@@ -170,6 +172,24 @@ __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *
   constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS, DB = Geo<D>::DB;
   const bool second = !MASK || (kb + 32 <= w.wave_last_key);
   f32x16 sacc[2];
+  if (!MASK) {
+    // all 16 K fragments of the tile in flight before the first MFMA
+    bf16x8 kf[2][DS];
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) kf[b2][ds] = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2) {
+      sacc[b2] = f32x16{};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds)
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[b2][ds], w.qf[ds], sacc[b2], 0, 0, 0);
+    }
+    // scheduling hint: the 16 LDS reads first, then the 16 MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS, 0);  // DS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * DS, 0);  // MFMA
+  } else {
 #pragma unroll
   for (int b2 = 0; b2 < 2; ++b2) {
     if (MASK && b2 == 1 && !second) {
@@ -182,6 +202,7 @@ __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *
     sacc[b2] = f32x16{};
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ds], w.qf[ds], sacc[b2], 0, 0, 0);
+  }
   }
   if (MASK) {
 #pragma unroll
