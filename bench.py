@@ -2,16 +2,19 @@
 
 One step is one pass of the whole hot path over one synthetic layer already
 resident in HBM: the important-row gather of the hidden states, then
-daf_layer_attn (hybrid KV write-back, stage 1 and stage 2 in one grid, split
-merge, fusion into the hidden states). W untimed warmup steps, then exactly K
+daf_layer_attn (hybrid KV write-back, stage 2 with its split merge, stage 1;
+both stages write their rows into the hidden states in their epilogues). W untimed warmup steps, then exactly K
 timed steps between device synchronisations. Several copies of the inputs are
 used in rotation so that consecutive steps do not find their data in the
 256 MB Infinity Cache.
 
 A second timed loop calls the stages one by one with HIP events between them
 (on the stream the kernels run on) for per-stage times, TFLOP/s, TB/s and the
-roofline fraction of the dominant kernel (stage 1). The CPU oracle is timed on
-the host on a bounded sample of the same layer (``cpu_baseline``).
+roofline fraction of the dominant kernel (stage 1). Its HBM traffic comes from
+the committed rocprofv3 counter summary when that summary was taken on the
+current attention sources (their SHA-256 is recorded there), else it is null.
+The CPU oracle is timed on the host on a bounded sample of the same layer
+(``cpu_baseline``).
 
 Prints one JSON line.
 """
@@ -34,6 +37,43 @@ METRIC = "DAF per-layer attention µs at L_d=32k,r=0.15; stage TFLOP/s + HBM TB/
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_stage1_qwen7b_32k_pmc.md")
+# sources whose change invalidates counter-measured traffic of the attention kernels
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_21599_amd", "csrc", f)
+                for f in ("attn_bf16.hip", "attn.hip", "api.hip", "daf_internal.h")] + [
+    os.path.join(ROOT, "paper_2607_21599_amd", "build.py")]
+
+
+def attn_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """Counter-measured HBM bytes per stage-1 launch from the committed
+    summary, or None if it is absent, for another workload, or was taken on
+    other attention sources."""
+    try:
+        with open(TRAFFIC_SUMMARY) as fh:
+            lines = fh.read().splitlines()
+    except OSError:
+        return None
+    fields = {}
+    for ln in lines:
+        if ln.startswith("traffic-record:"):
+            for kv in ln.split(":", 1)[1].split():
+                k, _, v = kv.partition("=")
+                fields[k] = v
+    if fields.get("workload") != workload or fields.get("sources_sha256") != attn_source_hash():
+        return None
+    try:
+        return int(fields["stage1_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def work(shapes) -> dict:
@@ -152,27 +192,32 @@ def main():
     ms_per_step = t0.elapsed_time(t1) / args.steps
     print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
-    # per-stage times: the same calls one by one, events on the launch stream
+    # Per-stage times: events around each stage call on the launch stream. A
+    # host call takes longer than the shorter kernels, so a GPU spin is queued
+    # before each timed call: the events and the call are all enqueued before
+    # the GPU reaches them, and the event pair measures the call's GPU time.
+    # The calls are idempotent (same inputs, same outputs).
     names = ["gather", "fuse_kv", "stage1", "stage2", "fuse_hidden"]
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
-    for i in range(args.steps):
-        b = bufs[i % len(bufs)]
-        g = gath[i % len(bufs)]
-        e = ev[i]
-        e[0].record()
-        b.gather_hidden(g)
-        e[1].record()
-        b.fuse_kv()
-        e[2].record()
-        b.stage1()
-        e[3].record()
-        b.stage2()
-        e[4].record()
-        b.fuse_hidden()
-        e[5].record()
-    torch.cuda.synchronize()
-    stage_us = {n: float(np.mean([ev[i][k].elapsed_time(ev[i][k + 1]) for i in range(args.steps)])) * 1e3
-                for k, n in enumerate(names)}
+    calls = {
+        "gather": lambda j: bufs[j].gather_hidden(gath[j]),
+        "fuse_kv": lambda j: bufs[j].fuse_kv(),
+        "stage1": lambda j: bufs[j].stage1(),
+        "stage2": lambda j: bufs[j].stage2(),
+        "fuse_hidden": lambda j: bufs[j].fuse_hidden(),
+    }
+    spin_cycles = 400_000  # ~0.2 ms at the MI355X shader clock, longer than a host call
+    stage_us = {}
+    for n in names:
+        calls[n](0)
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for i in range(args.steps):
+            torch.cuda._sleep(spin_cycles)
+            ev[i][0].record()
+            calls[n](i % len(bufs))
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        stage_us[n] = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
     wk = work(shapes)
     peak_mma = PEAK_BF16_TFLOPS if s0.dtype == di.BF16 else PEAK_F32_TFLOPS
 
@@ -207,9 +252,10 @@ def main():
         t_floor = max(st["flop"] / (peak_mma * 1e12), st["bytes"] / (PEAK_HBM_GBS * 1e9))
         st["roofline_frac"] = t_floor / (st["us"] * 1e-6)
     s1 = stages["stage1_imp_self_attn"]
-    roofline = dict(bound="mfma", kernel="attn_fwd_kernel (stage 1, daf_imp_self_attn)",
+    roofline = dict(bound="mfma", kernel="attn_bf16_kernel<128,0> (stage 1, daf_imp_self_attn)",
                     achieved=s1["TFLOPs"], peak=peak_mma, unit="TFLOP/s", frac=s1["TFLOPs"] / peak_mma,
-                    traffic=None, flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
+                    traffic=measured_traffic(args.workload), traffic_unit="bytes per launch (HBM, counters)",
+                    flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
 
     out = {
         "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,

@@ -174,11 +174,11 @@ size_t daf_layer_workspace_size(const daf_attn_cfg_t *cfg,
                                 const daf_batch_t *batch);
 
 /* One DAF attention layer (Sec. 2 items 1-3), in the order the paper fixes:
- * hybrid KV write-back (DAF_FUSE_KV) first, then stage 1 and stage 2 (one
- * grid), then the state fusion, all on `stream`. Arguments as in the stage
- * calls. o_imp and o_q receive the stage outputs; the same rows are written
- * into `hidden` exactly as DAF_FUSE_HIDDEN would (the fusion happens in the
- * stage epilogues, without a separate pass). */
+ * hybrid KV write-back (DAF_FUSE_KV) first, then stage 2 (with its split
+ * merge) and stage 1, all on `stream`. Arguments as in the stage calls. o_imp
+ * and o_q receive the stage outputs; the same rows are written into `hidden`
+ * exactly as DAF_FUSE_HIDDEN would (the state fusion happens in the stage
+ * epilogues, without a separate pass). */
 daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
                             const int32_t *idx, const void *q_imp,
                             const void *k_imp, const void *v_imp,
