@@ -19,10 +19,13 @@
 //    operand (8 consecutive keys of one feature per lane) is read from the
 //    row-major V tile with ds_read_b64_tr_b16, which transposes 16-bit data
 //    across each 16-lane group.
-//  * Online softmax in fp32, base 2, per 32-key half tile. The running max is
-//    only raised when a row's max grows by more than 2^8 (probabilities stay
-//    <= 256, exact in fp32 and bf16 range), so the O rescale is almost always
-//    skipped; the row max of a lane pair is exchanged with v_permlane32_swap.
+//  * Online softmax in fp32, base 2. Full tiles keep the running max per
+//    32-key half, so the S MFMAs of half 1 overlap the softmax of half 0 and
+//    the P.V MFMAs of half 0 overlap the max of half 1; diagonal tiles take one
+//    max over the tile. The running max is only raised when a row's max grows
+//    by more than 2^8 (probabilities stay <= 256, exact in fp32 and bf16
+//    range), so the O rescale is almost always skipped; the row max of a lane
+//    pair is exchanged with v_permlane32_swap.
 #include <math.h>
 
 #include "daf_internal.h"
@@ -163,36 +166,67 @@ __device__ __forceinline__ void pv_half(WaveState<D> &w, const unsigned char *vs
     for (int db = 0; db < DB; ++db) w.oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[c][db], pf[c], w.oacc[db], 0, 0, 0);
 }
 
-// One 64-key tile: S^T = K Q^T, online softmax (one max per tile), O^T update.
-// MASK selects the diagonal-tile variant (causal mask, possibly a fully masked
-// second half); full tiles run straight-line code so the scheduler can overlap
-// the P.V MFMAs of one half with the softmax of the other.
+// Raise the running max if this half's max grew by more than the slack
+// (wave-uniform decision), rescaling O and the row sum.
+template <int D>
+__device__ __forceinline__ void maybe_raise(WaveState<D> &w, float mt) {
+  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(w.m_run, mt);
+    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
+    w.m_run = m_new;
+    w.l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < Geo<D>::DB; ++db) w.oacc[db] *= alpha;
+  }
+}
+template <int D>
+__device__ __forceinline__ float half_max(const WaveState<D> &w, const f32x16 &sacc) {
+  float mx = sacc[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+  return pair_max(mx) * w.sl2;
+}
+
+// One 64-key tile: S^T = K Q^T, online softmax, O^T update. MASK selects the
+// diagonal-tile variant (causal mask, possibly a fully masked second half).
+// Full tiles keep one running max per 32-key half, so the S MFMAs of half 1
+// overlap the softmax of half 0 and the P.V MFMAs of half 0 overlap the max of
+// half 1.
 template <int D, bool MASK>
 __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *ks, const unsigned char *vs, int kb) {
   constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS, DB = Geo<D>::DB;
-  const bool second = !MASK || (kb + 32 <= w.wave_last_key);
-  f32x16 sacc[2];
   if (!MASK) {
-    // all 16 K fragments of the tile in flight before the first MFMA
     bf16x8 kf[2][DS];
 #pragma unroll
     for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) kf[b2][ds] = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
+    f32x16 s0 = f32x16{};
 #pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2) {
-      sacc[b2] = f32x16{};
+    for (int ds = 0; ds < DS; ++ds) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0][ds], w.qf[ds], s0, 0, 0, 0);
+    const float mt0 = half_max<D>(w, s0);
+    // scheduling hint: all K reads first, then the S MFMAs of half 0
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, DS, 0);
+    maybe_raise<D>(w, mt0);
+    f32x16 s1 = f32x16{};
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds)
-        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[b2][ds], w.qf[ds], sacc[b2], 0, 0, 0);
-    }
-    // scheduling hint: the 16 LDS reads first, then the 16 MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS, 0);  // DS reads
-    __builtin_amdgcn_sched_group_barrier(0x008, 2 * DS, 0);  // MFMA
-  } else {
+    for (int ds = 0; ds < DS; ++ds) s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[1][ds], w.qf[ds], s1, 0, 0, 0);
+    bf16x8 pf0[2];
+    softmax_half<D>(w, s0, w.m_run, pf0);
+    pv_half<D>(w, vs, pf0);
+    const float mt1 = half_max<D>(w, s1);
+    maybe_raise<D>(w, mt1);
+    bf16x8 pf1[2];
+    softmax_half<D>(w, s1, w.m_run, pf1);
+    pv_half<D>(w, vs + 32 * ROWB, pf1);
+    return;
+  }
+  const bool second = kb + 32 <= w.wave_last_key;
+  f32x16 sacc[2];
 #pragma unroll
   for (int b2 = 0; b2 < 2; ++b2) {
-    if (MASK && b2 == 1 && !second) {
+    if (b2 == 1 && !second) {
       sacc[1] = f32x16{};
       continue;
     }
@@ -203,29 +237,18 @@ __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ds], w.qf[ds], sacc[b2], 0, 0, 0);
   }
-  }
-  if (MASK) {
 #pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2) {
+  for (int b2 = 0; b2 < 2; ++b2) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb + 32 * b2 + 8 * (r >> 2) + 4 * w.half + (r & 3);
-        if (key > w.limit) sacc[b2][r] = -INFINITY;
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int key = kb + 32 * b2 + 8 * (r >> 2) + 4 * w.half + (r & 3);
+      if (key > w.limit) sacc[b2][r] = -INFINITY;
     }
   }
   float mx = fmaxf(sacc[0][0], sacc[1][0]);
 #pragma unroll
   for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sacc[0][r], sacc[1][r]));
-  const float mt = pair_max(mx) * w.sl2;
-  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
-    const float m_new = fmaxf(w.m_run, mt);
-    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
-    w.m_run = m_new;
-    w.l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) w.oacc[db] *= alpha;
-  }
+  maybe_raise<D>(w, pair_max(mx) * w.sl2);
   const float m_use = (w.m_run == -INFINITY) ? 0.f : w.m_run;
   bf16x8 pf0[2], pf1[2];
   softmax_half<D>(w, sacc[0], m_use, pf0);
