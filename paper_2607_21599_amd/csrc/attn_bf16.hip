@@ -38,6 +38,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
@@ -117,6 +118,30 @@ __device__ __forceinline__ void dma_tile(const unsigned char *kg, const unsigned
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (void __attribute__((address_space(3))) *)(vbase + i * 1024), 16,
                                              dma_v[i], 0, 0, 0);
 #endif
+}
+
+// Output staging: 32 rows of ROWB bytes per wave in LDS, the 16-byte chunks of
+// a row XOR-swizzled by the row so that both the per-lane writes (pieces of
+// every chunk of one row) and the row-contiguous reads spread over the banks.
+// stage_put writes v (8 or 16 bytes) at byte `sub` of logical chunk c of row r.
+template <int D, typename V>
+__device__ __forceinline__ void stage_put(unsigned char *stg, int r, int c, int sub, const V &v) {
+  constexpr int CH = Geo<D>::CH;
+  *reinterpret_cast<V *>(stg + r * Geo<D>::ROWB + ((c ^ (r & (CH - 1))) << 4) + sub) = v;
+}
+// Write the wave's staged rows wrow .. wrow+31 (those below n_rows): each lane
+// moves one 16-byte chunk, CH lanes cover a row, so every store instruction
+// writes 64/CH whole rows. dst(r) is the byte address of row r's first chunk.
+template <int D, typename F>
+__device__ __forceinline__ void store_rows(const unsigned char *stg, int lane, int wrow, int n_rows, F dst) {
+  constexpr int CH = Geo<D>::CH, RPL = 64 / CH;
+  const int j = lane % CH;
+#pragma unroll
+  for (int it = 0; it < 32 / RPL; ++it) {
+    const int r = it * RPL + lane / CH;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(stg + r * Geo<D>::ROWB + ((j ^ (r & (CH - 1))) << 4));
+    if (wrow + r < n_rows) *reinterpret_cast<u32x4 *>(dst(wrow + r) + j * 16) = v;
+  }
 }
 
 // Per-wave state of one workgroup tile (lives in registers after inlining).
@@ -397,40 +422,52 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   const float l_tot = pair_sum(w.l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_nat = l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-  if (my_row >= n_rows) return;
+  // Rows go out through LDS so that every store is a 16-byte piece of a
+  // contiguous row (a lane holds 4-feature pieces of one row, spread over the
+  // row). Each wave stages in its own quarter of the stage buffer that did
+  // not hold the last tile: every wave finished reading it before the last
+  // barrier and no copy targets it any more.
+  unsigned char *stg = ((n_tiles & 1) ? (wave < 2 ? k_lds1 : v_lds1) : (wave < 2 ? k_lds0 : v_lds0)) +
+                       (wave & 1) * (TILE / 2);
+  const int wrow = row0 + wave * 32;  // first row of this wave
   if (E.n_splits == 1 && E.o != nullptr) {
-    __bf16 *op = static_cast<__bf16 *>(E.o) + ((size_t)my_row * p.hq + h) * D + 4 * half;
-    __bf16 *op2 = nullptr;
-    if (E.o2 != nullptr) {
-      const int64_t r2 = E.o2_row0 + (E.o2_idx ? E.o2_idx[my_row] : my_row);
-      op2 = static_cast<__bf16 *>(E.o2) + ((size_t)r2 * p.hq + h) * D + 4 * half;
-    }
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         bf16x4 v;
 #pragma unroll
         for (int t = 0; t < 4; ++t) v[t] = (__bf16)(w.oacc[db][4 * q4 + t] * inv);
-        *reinterpret_cast<bf16x4 *>(op + db * 32 + 8 * q4) = v;
-        if (op2) *reinterpret_cast<bf16x4 *>(op2 + db * 32 + 8 * q4) = v;
+        stage_put<D>(stg, l32, 4 * db + q4, 8 * half, v);
       }
-    }
-    if (E.lse != nullptr && half == 0) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
+    store_rows<D>(stg, lane, wrow, n_rows, [&](int r) {
+      return static_cast<unsigned char *>(E.o) + ((size_t)r * p.hq + h) * D * 2;
+    });
+    if (E.o2 != nullptr)
+      store_rows<D>(stg, lane, wrow, n_rows, [&](int r) {
+        const int64_t r2 = E.o2_row0 + (E.o2_idx ? E.o2_idx[r] : r);
+        return static_cast<unsigned char *>(E.o2) + ((size_t)r2 * p.hq + h) * D * 2;
+      });
+    if (E.lse != nullptr && half == 0 && my_row < n_rows) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
   } else {
-    const size_t prow = (size_t)my_row * E.n_splits + s;
-    float *op = E.part_o + (prow * p.hq + h) * D + 4 * half;
+    // fp32 partials: two passes over half the features each (ROWB bytes per row)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        f32x4 v;
+      for (int db2 = 0; db2 < DB / 2; ++db2)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[t] = w.oacc[db][4 * q4 + t] * inv;
-        *reinterpret_cast<f32x4 *>(op + db * 32 + 8 * q4) = v;
-      }
+        for (int q4 = 0; q4 < 4; ++q4) {
+          f32x4 v;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = w.oacc[pass * (DB / 2) + db2][4 * q4 + t] * inv;
+          stage_put<D>(stg, l32, 8 * db2 + 2 * q4 + half, 0, v);
+        }
+      store_rows<D>(stg, lane, wrow, n_rows, [&](int r) {
+        const size_t prow = (size_t)r * E.n_splits + s;
+        return reinterpret_cast<unsigned char *>(E.part_o + (prow * p.hq + h) * D) + pass * Gm::ROWB;
+      });
     }
-    if (half == 0) E.part_lse[prow * p.hq + h] = lse_nat;
+    if (half == 0 && my_row < n_rows) E.part_lse[((size_t)my_row * E.n_splits + s) * p.hq + h] = lse_nat;
   }
 }
 
