@@ -19,6 +19,11 @@ the order the paper gives (Sec. 2):
   4. state fusion: stage outputs written into the hidden-state rows of their
      tokens (Sec. 2 item 3).
 
+For the comparison with the schemes the Complexity Analysis contrasts DAF
+with, it also gives full recomputation (causal attention over every token) and
+the CacheBlend pattern (important and question tokens over the full context,
+causal by original position).
+
 Arrays are numpy. Raw buffers (bf16 bit patterns as uint16, or float32) are
 moved byte for byte; attention inputs are float32 and outputs are float64.
 Parity is pinned by the CPU test suite (closed forms, library reductions,
@@ -75,6 +80,7 @@ class Oracle:
         lib.daf_oracle_scatter_rows.argtypes = [_u8p, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
         lib.daf_oracle_mask_stage1.argtypes = [_i64p, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
         lib.daf_oracle_mask_stage2.argtypes = [ctypes.c_int64, ctypes.c_int64, _i64p, ctypes.c_int64, _u8p]
+        lib.daf_oracle_mask_position.argtypes = [_i64p, _i64p, ctypes.c_int64, ctypes.c_int64, _u8p]
         lib.daf_oracle_masked_attention.argtypes = [
             _f32p, _f32p, _f32p, _u8p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
             ctypes.c_int32, ctypes.c_double, _i64p, ctypes.c_int64, _f64p, _f64p, _f64p]
@@ -128,6 +134,15 @@ class Oracle:
         mask = np.zeros((len(r), L_d + L_q), dtype=np.uint8)
         if len(r):
             self.lib.daf_oracle_mask_stage2(L_d, L_q, _ptr(r, _i64p), len(r), _ptr(mask, _u8p))
+        return mask
+
+    def mask_position(self, qpos, nk: int, rows=None) -> np.ndarray:
+        qpos = np.ascontiguousarray(np.asarray(qpos, dtype=np.int64))
+        r = _rows_arg(rows, len(qpos))
+        mask = np.zeros((len(r), nk), dtype=np.uint8)
+        if len(r) and nk:
+            self.lib.daf_oracle_mask_position(_ptr(qpos, _i64p), _ptr(r, _i64p), len(r), nk,
+                                              _ptr(mask, _u8p))
         return mask
 
     # ---- attention ----------------------------------------------------------
@@ -190,6 +205,29 @@ class Oracle:
         L_q = q_q.shape[0]
         mask = self.mask_stage2(L_d, L_q, rows)
         return self.attention(q_q, k_hyb, v_hyb, mask, scale, rows, want_p)
+
+    # ---- comparison patterns (Complexity Analysis) ----------------------------
+    def position_attention(self, q, k, v, qpos, scale, rows=None, want_p=False):
+        """Queries at original positions qpos over a key sequence, each seeing
+        the keys at positions 0..qpos (causal by position)."""
+        mask = self.mask_position(qpos, k.shape[0], rows)
+        return self.attention(q, k, v, mask, scale, rows, want_p)
+
+    def full_recompute(self, q, k, v, scale, rows=None):
+        """Full recomputation: causal attention over every token of the
+        sequence with fresh Q/K/V (the r = 1 case of the comparison)."""
+        return self.position_attention(q, k, v, np.arange(q.shape[0]), scale, rows)
+
+    def cacheblend(self, q_imp, q_q, k_hyb, v_hyb, idx, L_d: int, scale, rows=None):
+        """The recomputation pattern the Complexity Analysis attributes to
+        CacheBlend: the important tokens and the question tokens attend over
+        the full context (the hybrid [L_d + L_q] cache), each causal by its
+        original position. Rows are the important rows, then the question."""
+        idx = np.asarray(idx, dtype=np.int64)
+        L_q = q_q.shape[0]
+        q = np.concatenate([np.asarray(q_imp, np.float32), np.asarray(q_q, np.float32)], axis=0)
+        qpos = np.concatenate([idx, L_d + np.arange(L_q, dtype=np.int64)])
+        return self.position_attention(q, k_hyb, v_hyb, qpos, scale, rows)
 
     def fuse_hidden(self, hidden, idx, o_imp, o_q, L_d: int):
         """State fusion (Sec. 2 item 3): hidden[idx[i]] = o_imp[i] and

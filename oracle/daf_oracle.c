@@ -117,6 +117,23 @@ void daf_oracle_mask_stage2(int64_t L_d, int64_t L_q, const int64_t *rows,
   }
 }
 
+/* Position-causal mask for the comparison patterns (Complexity Analysis:
+ * recomputation schemes in which the recomputed tokens and the question attend
+ * over the full context). Query row r sits at original position qpos[rows[r]]
+ * of a key sequence of nk tokens and sees keys 0..qpos. mask is [nrows][nk],
+ * 1 = visible. With qpos[i] = i this is plain causal attention over the whole
+ * sequence (full recomputation). */
+void daf_oracle_mask_position(const int64_t *qpos, const int64_t *rows,
+                              int64_t nrows, int64_t nk, uint8_t *mask) {
+  for (int64_t r = 0; r < nrows; ++r) {
+    int64_t p = qpos[rows[r]];
+#if DAF_ORACLE_MUTANT == 12
+    p += 1; /* planted: one key past the query's own position visible */
+#endif
+    for (int64_t k = 0; k < nk; ++k) mask[r * nk + k] = (uint8_t)(k <= p);
+  }
+}
+
 /* Scaled dot-product attention with an explicit mask, by definition.
  *
  *   q: [nq][hq][d] float32 (only rows listed in `rows` are used)

@@ -345,9 +345,58 @@ def pin_brute_force_subsets(orc):
             _close(out["o_q"], ref, what=f"subset {sub} stage2")
 
 
+def pin_full_recompute_patterns(orc):
+    """Comparison pattern 1 (full recomputation): causal attention over every
+    token of the sequence, equal to torch's causal SDPA (GQA 7:1)."""
+    rng = _rng(31)
+    L, hq, hkv, d = 41, 7, 1, 16
+    q, k, v = _randn(rng, L, hq, d), _randn(rng, L, hkv, d), _randn(rng, L, hkv, d)
+    o, _ = orc.full_recompute(q, k, v, 0.3)
+    _close(o, sdpa_causal(q, k, v, 0.3), what="full recompute")
+
+
+def pin_cacheblend_rows(orc):
+    """Comparison pattern 2 (the CacheBlend recomputation the Complexity
+    Analysis describes): important and question tokens over the full hybrid
+    context are the rows idx and L_d + j of one causal attention over the
+    whole sequence whose queries at those positions are q_imp and q_q."""
+    rng = _rng(32)
+    L_d, L_q, hq, hkv, d = 31, 6, 4, 2, 16
+    x = _sparse_layer_inputs(rng, L_d, L_q, 11, hq, hkv, d)
+    kh, vh = orc.hybrid_kv(x["k_cache"], x["v_cache"], x["idx"], x["k_imp"], x["v_imp"],
+                           x["k_q"], x["v_q"], L_d)
+    o, _ = orc.cacheblend(x["q_imp"], x["q_q"], kh, vh, x["idx"], L_d, 0.4)
+    q_full = _randn(rng, L_d + L_q, hq, d)
+    q_full[x["idx"]] = x["q_imp"]
+    q_full[L_d:] = x["q_q"]
+    ke, ve = x["k_cache"].copy(), x["v_cache"].copy()
+    ke[x["idx"]], ve[x["idx"]] = x["k_imp"], x["v_imp"]
+    ke[L_d:], ve[L_d:] = x["k_q"], x["v_q"]
+    ref = sdpa_causal(q_full, ke, ve, 0.4)
+    rows = np.concatenate([x["idx"], L_d + np.arange(L_q)])
+    _close(o, ref[rows], what="cacheblend rows")
+
+
+def pin_position_zero_queries(orc):
+    """Zero queries at sorted positions p: each output row is the mean of the
+    value rows 0..p and lse = ln(p + 1) (closed form)."""
+    rng = _rng(33)
+    nk, hq, hkv, d = 23, 2, 1, 8
+    v = _randn(rng, nk, hkv, d)
+    k = _randn(rng, nk, hkv, d)
+    qpos = np.array([0, 3, 4, 10, 22])
+    q = np.zeros((len(qpos), hq, d), np.float32)
+    o, lse = orc.position_attention(q, k, v, qpos, 1.0)
+    for i, p in enumerate(qpos):
+        for h in range(hq):
+            _close(o[i, h], v[: p + 1, 0].astype(np.float64).mean(axis=0), what="position mean")
+            _close(lse[i, h], math.log(p + 1), what="position lse")
+
+
 ALL_PINS = [
     pin_hand_two_tokens, pin_stage1_full_recompute, pin_stage1_condensed,
     pin_stage1_position_order, pin_hybrid_cache, pin_stage2_concat, pin_constant_values,
     pin_zero_queries, pin_gqa_groups, pin_needle, pin_probabilities, pin_layer_independence,
     pin_layer_full_recompute, pin_gather_scatter, pin_fuse_rows, pin_brute_force_subsets,
+    pin_full_recompute_patterns, pin_cacheblend_rows, pin_position_zero_queries,
 ]

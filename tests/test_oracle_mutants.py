@@ -4,7 +4,8 @@ Each C mutant is a build of ``oracle/daf_oracle.c`` with one mistake compiled
 in (a dropped scale, an interleaved GQA map, a mask by storage order instead
 of position, a non-causal question block, K read as V, lse without the max, a
 term dropped from the softmax sum, a lost gather row, reversed scatter sources,
-the question's own key dropped, a feature dropped from the dot product). The
+the question's own key dropped, a feature dropped from the dot product, a
+position mask one key too wide). The
 Python plants skip the hybrid write-back, leave the question K/V out of the
 cache, or fuse question rows one row early.
 """
@@ -16,7 +17,7 @@ import oracle as orc_mod
 from oracle import build as orc_build
 from oracle_pins import ALL_PINS
 
-C_MUTANTS = list(range(1, 12))
+C_MUTANTS = list(range(1, 13))
 PY_PLANTS = ["no_hybrid", "no_question_kv", "fuse_shift"]
 
 
