@@ -206,6 +206,14 @@ def make_request(s: Shape) -> dict:
     return r
 
 
+def make_full_queries(s: Shape) -> np.ndarray:
+    """Queries for every token of a request ([T, hq, d], raw), for the
+    full-recomputation comparison pattern: drawn from their own stream
+    (seed + 7919) with the request's query distribution."""
+    rng = np.random.Generator(np.random.PCG64(s.seed + 7919))
+    return _normal(rng, (s.T, s.hq, s.d), s.qkv_std, s.dtype)
+
+
 @dataclass
 class Batch:
     """Requests concatenated along the token axis, with prefix offsets.

@@ -133,6 +133,26 @@ daf_status_t daf_imp_self_attn(const daf_attn_cfg_t *cfg,
                                const void *k_imp, const void *v_imp,
                                void *o_imp, float *lse_imp, hipStream_t stream);
 
+/* Attention of queries at given positions of a key sequence, for the
+ * comparison the Complexity Analysis draws: schemes that recompute selected
+ * tokens and the question over the full context (the CacheBlend pattern:
+ * important and question tokens over all L_d + L_q keys, O(r L_d^2 + L_d L_q))
+ * and full recomputation (every token over its prefix), against which DAF's
+ * O(r^2 L_d^2 + L_q (L_d + L_q)) is measured; the Hardware Compatibility
+ * paragraph notes that such unified recomputation needs non-standard masks.
+ *   q [n_rows][Hq][D], k / v [n_keys][Hkv][D] -> o [n_rows][Hq][D];
+ *   lse: nullable float32 [Hq][n_rows].
+ * Row i sees keys 0 .. q_pos[i]; q_pos (DEVICE int32 [n_rows]) must be
+ * strictly increasing with values in [0, n_keys) - not checked, violations are
+ * undefined behaviour. q_pos = NULL means bottom-right causal: row i sees keys
+ * 0 .. i + n_keys - n_rows (requires n_rows <= n_keys); with n_rows = n_keys
+ * that is full causal self-attention. One sequence per call; no workspace. */
+daf_status_t daf_position_attn(const daf_attn_cfg_t *cfg, int32_t n_rows,
+                               int32_t n_keys, const void *q,
+                               const int32_t *q_pos, const void *k,
+                               const void *v, void *o, float *lse,
+                               hipStream_t stream);
+
 /* Bytes of workspace daf_qdoc_attn needs for this shape (0 on bad input). */
 size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg,
                                const daf_batch_t *batch);

@@ -16,7 +16,7 @@ import numpy as np
 __all__ = [
     "DAF_OK", "DAF_BF16", "DAF_F32", "DAF_SRC_TOKENS", "DAF_SRC_DOCS", "DAF_FUSE_KV",
     "DAF_FUSE_HIDDEN", "DafError", "AttnCfg", "Batch", "lib", "library_path",
-    "daf_gather_important", "daf_imp_self_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
+    "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices",
     "daf_status_string", "daf_last_error", "daf_version", "EXPORTED",
 ]
@@ -29,7 +29,7 @@ DAF_FUSE_KV, DAF_FUSE_HIDDEN = 1, 2
 
 # every symbol include/daf.h declares
 EXPORTED = [
-    "daf_gather_important", "daf_imp_self_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
+    "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices",
     "daf_status_string", "daf_last_error", "daf_version",
 ]
@@ -92,6 +92,8 @@ def lib() -> ctypes.CDLL:
         sig = {
             "daf_gather_important": (i32, [bp, i32, _vp, i64, _vp, _vp, _vp]),
             "daf_imp_self_attn": (i32, [cfgp, bp, _vp, _vp, _vp, _vp, _vp, _vp]),
+            "daf_position_attn": (i32, [cfgp, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                        _vp]),
             "daf_qdoc_workspace_size": (sz, [cfgp, bp]),
             "daf_qdoc_attn": (i32, [cfgp, bp, _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp]),
             "daf_fuse": (i32, [cfgp, bp, u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -157,6 +159,11 @@ def daf_imp_self_attn(cfg: AttnCfg, batch: Batch, q_imp, k_imp, v_imp, o_imp, ls
                       stream=None):
     _check(lib().daf_imp_self_attn(_cfgp(cfg), _bp(batch), _ptr(q_imp), _ptr(k_imp), _ptr(v_imp),
                                    _ptr(o_imp), _ptr(lse_imp), _stream(stream)))
+
+
+def daf_position_attn(cfg: AttnCfg, n_rows: int, n_keys: int, q, q_pos, k, v, o, lse=None, stream=None):
+    _check(lib().daf_position_attn(_cfgp(cfg), n_rows, n_keys, _ptr(q), _ptr(q_pos), _ptr(k), _ptr(v),
+                                   _ptr(o), _ptr(lse), _stream(stream)))
 
 
 def daf_qdoc_workspace_size(cfg: AttnCfg, batch: Batch) -> int:

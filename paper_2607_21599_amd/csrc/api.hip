@@ -470,6 +470,48 @@ daf_status_t daf_imp_self_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *bat
   }
 }
 
+daf_status_t daf_position_attn(const daf_attn_cfg_t *cfg, int32_t n_rows, int32_t n_keys, const void *q,
+                               const int32_t *q_pos, const void *k, const void *v, void *o, float *lse,
+                               hipStream_t stream) {
+  try {
+    Cfg c;
+    CHECK(parse_cfg(cfg, c));
+    if (n_rows < 0 || n_keys < 0) return fail(DAF_ERR_INVALID_ARG, "n_rows=%d, n_keys=%d must be >= 0", n_rows, n_keys);
+    if (!q_pos && n_rows > n_keys)
+      return fail(DAF_ERR_INVALID_ARG, "without q_pos, n_rows=%d must not exceed n_keys=%d", n_rows, n_keys);
+    if (q_pos && n_rows > 0 && n_keys == 0) return fail(DAF_ERR_INVALID_ARG, "n_keys is 0 but rows have positions");
+    if ((int64_t)n_keys * c.hkv * c.d * c.elem > INT32_MAX)
+      return fail(DAF_ERR_UNSUPPORTED, "%lld K/V bytes exceed 2 GiB", (long long)n_keys * c.hkv * c.d * c.elem);
+    if (n_rows == 0) return ok();
+    CHECK(need_ptr(q, "q"));
+    CHECK(need_ptr(k, "k"));
+    CHECK(need_ptr(v, "v"));
+    CHECK(need_ptr(o, "o"));
+    if (lse) CHECK(need_ptr(lse, "lse"));
+    if (q_pos && reinterpret_cast<uintptr_t>(q_pos) % 4 != 0) return fail(DAF_ERR_ALIGNMENT, "q_pos is not 4-byte aligned");
+    AttnEntry e{};
+    e.q = q;
+    e.k = k;
+    e.v = v;
+    e.o = o;
+    e.lse = lse;
+    e.lse_stride = n_rows;
+    e.n_rows = n_rows;
+    e.n_keys = n_keys;
+    const int mbs = (n_rows + kAttnBM - 1) / kAttnBM;
+    e.mb_hi = mbs - 1;
+    e.mb_count = mbs;
+    e.n_splits = 1;
+    e.split_keys = (n_keys + c.key_tile - 1) / c.key_tile * c.key_tile;
+    e.q_pos = q_pos;
+    std::vector<AttnEntry> entries{e};
+    CHECK(run_entries(c, AttnKind::kSelf, entries, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
 size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg, const daf_batch_t *batch) {
   try {
     Cfg c;

@@ -115,11 +115,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
   const int h = g * G + hl;
 
   const int n_rows = E.n_rows;
-  const int offset = E.n_keys - n_rows;
   const int row0 = mb * kAttnBM;
   const int row_last = min(row0 + kAttnBM, n_rows) - 1;
   const int k_begin = s * E.split_keys;
-  const int k_end = min(min(k_begin + E.split_keys, E.n_keys), row_last + offset + 1);
+  const int k_end = min(min(k_begin + E.split_keys, E.n_keys), row_limit(E, row_last) + 1);
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -207,7 +206,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
   float l_run = 0.f;        // this lane's share of the row sum
 
   const float sl2 = p.scale_log2;
-  const int limit = my_row + offset;  // last visible key of this lane's row
+  const int limit = row_limit(E, my_row);  // last visible key of this lane's row
+  const int wave_first_limit = row_limit(E, wrow0);  // keys up to this are visible to every row
 
   if (k_begin < k_end) load_tile(k_begin);
   for (int kb = k_begin; kb < k_end; kb += BN) {
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
     }
 
     // scale, causal mask, row max
-    const bool need_mask = (kb + BN - 1) > (wrow0 + offset);
+    const bool need_mask = (kb + BN - 1) > wave_first_limit;
     float mloc = -INFINITY;
 #pragma unroll
     for (int b2 = 0; b2 < NKB; ++b2) {

@@ -347,11 +347,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
 
   const int n_rows = E.n_rows;
   const int n_keys = E.n_keys;
-  const int offset = n_keys - n_rows;
   const int row0 = mb * kAttnBM;
   const int row_last = min(row0 + kAttnBM, n_rows) - 1;
   const int k_begin = s * E.split_keys;
-  const int k_end = min(min(k_begin + E.split_keys, n_keys), row_last + offset + 1);
+  const int k_end = min(min(k_begin + E.split_keys, n_keys), row_limit(E, row_last) + 1);
   const int n_tiles = k_end > k_begin ? (k_end - k_begin + kBN - 1) / kBN : 0;
 
   const int tid = threadIdx.x;
@@ -361,16 +360,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   const int half = lane >> 5;
   const int wrow0 = row0 + wave * 32;
   const int my_row = wrow0 + l32;
-  const int wave_last_key = wrow0 + 31 + offset;  // keys above this are masked for the whole wave
+  // keys above this are masked for the whole wave (a wave past the last row has none)
+  const int wave_last_key = wrow0 < n_rows ? row_limit(E, wrow0 + 31) : -1;
 
   WaveState<D> w;
   w.kg = static_cast<const unsigned char *>(E.k);
   w.vg = static_cast<const unsigned char *>(E.v);
   w.n_keys = n_keys;
   w.kv_row_bytes = p.hkv * D * 2;
-  w.limit = my_row + offset;
+  w.limit = row_limit(E, my_row);
   w.wave_last_key = wave_last_key;
-  w.wave_first_limit = wrow0 + offset;
+  w.wave_first_limit = row_limit(E, wrow0);
   w.half = half;
   w.wave = wave;
   w.sl2 = p.scale_log2;

@@ -18,7 +18,8 @@ constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident attention workgr
 // contiguous range of 128-row query blocks. Query row i (0-based in the
 // entry's request) sees keys 0 .. i + (n_keys - n_rows): causal, aligned to the
 // bottom right, which covers both DAF stages (stage 1: n_keys == n_rows;
-// stage 2: n_keys = L_d + L_q, n_rows = L_q).
+// stage 2: n_keys = L_d + L_q, n_rows = L_q). With q_pos set, row i sees keys
+// 0 .. q_pos[i] (queries at given positions of the key sequence).
 struct AttnEntry {
   const void *q;   // [n_rows][Hq][D], row 0 of the request
   const void *k;   // [n_keys][Hkv][D]
@@ -40,7 +41,17 @@ struct AttnEntry {
   void *o2;
   const int32_t *o2_idx;
   int64_t o2_row0;
+  // optional query positions: row i sees keys 0 .. q_pos[i] (strictly
+  // increasing, < n_keys) instead of 0 .. i + (n_keys - n_rows)
+  const int32_t *q_pos;
 };
+
+// Last key visible to query row r of entry e; rows past the end take the last
+// row's limit (their outputs are never written).
+__device__ __forceinline__ int row_limit(const AttnEntry &e, int r) {
+  const int rr = min(r, e.n_rows - 1);
+  return e.q_pos ? e.q_pos[rr] : rr + (e.n_keys - e.n_rows);
+}
 
 struct AttnLaunch;
 static_assert(sizeof(AttnEntry) * kMaxEntries + 64 < 4096, "attention launch table must fit 4 KiB of kernel arguments");

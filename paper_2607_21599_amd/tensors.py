@@ -13,7 +13,7 @@ import torch
 
 from . import (DAF_BF16, DAF_F32, DAF_FUSE_HIDDEN, DAF_FUSE_KV, DAF_SRC_TOKENS, AttnCfg, Batch,
                daf_fuse, daf_gather_important, daf_imp_self_attn, daf_layer_attn,
-               daf_layer_workspace_size, daf_qdoc_attn, daf_qdoc_workspace_size)
+               daf_layer_workspace_size, daf_position_attn, daf_qdoc_attn, daf_qdoc_workspace_size)
 
 
 def to_device(raw: np.ndarray, device="cuda") -> torch.Tensor:
@@ -94,3 +94,35 @@ class LayerBuffers:
         daf_layer_attn(self.cfg, self.batch, t["idx"], t["q_imp"], t["k_imp"], t["v_imp"], t["q_q"],
                        t["k_q"], t["v_q"], t["k_cache"], t["v_cache"], t["o_imp"], t["lse_imp"],
                        t["o_q"], t["lse_q"], t["hidden"], t["ws"], self.ws_bytes, stream)
+
+    # -- comparison patterns of one request --------------------------------------
+    def prepare_patterns(self, q_full: np.ndarray | None = None):
+        """Buffers of the comparison patterns (one request): the CacheBlend
+        queries (important rows, then the question rows) with their original
+        positions, and, if given, queries for every token (full recompute)."""
+        assert len(self.batch.cu_doc) == 2, "the comparison patterns take one request"
+        t = self.t
+        L_d, L_q = int(self.batch.cu_doc[1]), int(self.batch.cu_q[1])
+        t["q_cb"] = torch.cat([t["q_imp"], t["q_q"]]).contiguous()
+        qpos = torch.arange(L_d, L_d + L_q, dtype=torch.int32, device=self.device)
+        t["pos_cb"] = torch.cat([t["idx"], qpos]).contiguous()
+        t["o_cb"] = torch.zeros_like(t["q_cb"])
+        t["lse_cb"] = torch.zeros((self.hq, t["q_cb"].shape[0]), dtype=torch.float32, device=self.device)
+        if q_full is not None:
+            t["q_full"] = to_device(q_full, self.device)
+            t["o_full"] = torch.zeros_like(t["q_full"])
+            t["lse_full"] = torch.zeros((self.hq, t["q_full"].shape[0]), dtype=torch.float32,
+                                        device=self.device)
+
+    def cacheblend(self, stream=None):
+        """Important and question rows over the whole cache, causal by position."""
+        t = self.t
+        daf_position_attn(self.cfg, t["q_cb"].shape[0], t["k_cache"].shape[0], t["q_cb"], t["pos_cb"],
+                          t["k_cache"], t["v_cache"], t["o_cb"], t["lse_cb"], stream)
+
+    def full_recompute(self, stream=None):
+        """Every token over its prefix of the cache (causal self-attention)."""
+        t = self.t
+        n = t["q_full"].shape[0]
+        daf_position_attn(self.cfg, n, n, t["q_full"], None, t["k_cache"], t["v_cache"], t["o_full"],
+                          t["lse_full"], stream)

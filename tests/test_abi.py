@@ -118,3 +118,26 @@ def test_empty_work_is_a_no_op():
     daf.daf_qdoc_attn(c, b, None, None, None, None, None, None, 0, 0)
     daf.daf_layer_attn(c, b, *([None] * 14), None, 0, 0)
     daf.daf_gather_important(b, daf.DAF_SRC_TOKENS, None, 16, None, None, 0)
+
+
+def test_position_attn_checks():
+    c = _cfg()
+    with pytest.raises(daf.DafError) as e:  # negative sizes
+        daf.daf_position_attn(c, -1, 10, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # bottom-right causal needs n_rows <= n_keys
+        daf.daf_position_attn(c, 11, 10, FAKE, None, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # positions without keys
+        daf.daf_position_attn(c, 3, 0, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_position_attn(c, 3, 10, FAKE, FAKE + 2, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_ALIGNMENT
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_position_attn(c, 3, 10, FAKE, FAKE, None, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # K/V of one call must fit 32-bit byte offsets
+        daf.daf_position_attn(c, 3, 1 << 22, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_UNSUPPORTED
+    daf.daf_position_attn(c, 0, 10, None, None, None, None, None, None, 0)  # no rows: no-op
