@@ -141,6 +141,8 @@ def main():
     ap.add_argument("--cpu-stride1", type=int, default=4)
     ap.add_argument("--cpu-stride2", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-patterns", action="store_true",
+                    help="skip the comparison patterns (CacheBlend-style and full recomputation attention)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "kernel that calibrates HBM byte counters)")
@@ -257,6 +259,46 @@ def main():
                     traffic=measured_traffic(args.workload), traffic_unit="bytes per launch (HBM, counters)",
                     flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
 
+    comparison = None
+    if not args.no_patterns and len(shapes) == 1:
+        # The schemes the Complexity Analysis compares DAF with, as attention on
+        # the same GPU: the CacheBlend pattern (important and question rows over
+        # the whole hybrid cache, causal by position) and full recomputation
+        # (every token over its prefix). Same spin + event timing per call.
+        print("[bench] comparison patterns", file=sys.stderr, flush=True)
+        pb = bufs[0]
+        pb.fuse_kv()
+        pb.prepare_patterns(di.make_full_queries(s0))
+        pat_us = {}
+        for n, fn in (("cacheblend", pb.cacheblend), ("full_recompute", pb.full_recompute)):
+            fn()
+            torch.cuda.synchronize()
+            reps = 5
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+            for i in range(reps):
+                torch.cuda._sleep(spin_cycles)
+                ev[i][0].record()
+                fn()
+                ev[i][1].record()
+            torch.cuda.synchronize()
+            pat_us[n] = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        idx = batch.request(0)["idx"].astype(np.int64)
+        pos = np.concatenate([idx, s0.L_d + np.arange(s0.L_q)])
+        f_cb = 4 * s0.d * s0.hq * int((pos + 1).sum())
+        f_full = 4 * s0.d * s0.hq * s0.T * (s0.T + 1) // 2
+        daf_us = stage_us["stage1"] + stage_us["stage2"]
+        comparison = {
+            "daf_attention_us": daf_us, "daf_attention_flop": wk["stage1_flop"] + wk["stage2_flop"],
+            "cacheblend_us": pat_us["cacheblend"], "cacheblend_flop": f_cb,
+            "cacheblend_TFLOPs": tflops(f_cb, pat_us["cacheblend"]),
+            "full_recompute_us": pat_us["full_recompute"], "full_recompute_flop": f_full,
+            "full_recompute_TFLOPs": tflops(f_full, pat_us["full_recompute"]),
+            "speedup_vs_cacheblend": pat_us["cacheblend"] / daf_us,
+            "speedup_vs_full_recompute": pat_us["full_recompute"] / daf_us,
+            "note": "attention only (stage 1 + stage 2 vs the same kernels with position masks); "
+                    "the paper's Table 1 speedups are end-to-end TTFT on an A100",
+        }
+
     out = {
         "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
@@ -270,6 +312,8 @@ def main():
         "stages": stages,
         "roofline": roofline,
     }
+    if comparison is not None:
+        out["comparison"] = comparison
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(batch, args.cpu_stride1, args.cpu_stride2)
