@@ -317,7 +317,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   // ---- which work -----------------------------------------------------------
   // A work group is the G heads that share one KV head, for one entry, query
   // block and key split. When Hkv divides the 8 XCDs, each XCD serves one KV
-  // head (8/Hkv XCDs per head), so every L2 holds the K/V of a single head;
+  // head (8/Hkv XCDs per head, dealt alternately a, b, b, a, ...), so every L2
+  // holds the K/V of a single head;
   // otherwise work groups are dealt to the XCDs round-robin. Within an XCD,
   // work groups run heaviest first, and the G heads of a work group are
   // consecutive workgroups of that XCD.
@@ -329,7 +330,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   if (kXcds % p.hkv == 0) {
     const int xph = kXcds / p.hkv;
     g = xcd / xph;
-    lam = (slot / G) * xph + xcd % xph;
+    // work groups of a head are dealt to its xph XCDs in boustrophedon order
+    // (a, b, b, a, ...), so the XCDs get equal shares of the heaviest-first list
+    const int q = slot / G, r = xcd % xph;
+    lam = q * xph + ((q & 1) ? xph - 1 - r : r);
     if (lam * p.hkv >= p.n_groups) return;
   } else {
     const int gamma = (slot / G) * kXcds + xcd;
