@@ -214,6 +214,23 @@ def make_full_queries(s: Shape) -> np.ndarray:
     return _normal(rng, (s.T, s.hq, s.d), s.qkv_std, s.dtype)
 
 
+def make_selection_inputs(s: Shape, n_layers: int = 3):
+    """Keys of the selection layers for every document token: the offline
+    cached keys and the freshly computed ones, [n_layers, L_d, hkv, d] raw
+    each. The fresh keys deviate from the cached ones by N(0,1) noise scaled
+    per token by a log-normal factor (exp(N(0, 0.5)) * 0.1), so that some
+    tokens deviate much more than others. Drawn from their own stream (seed +
+    104729)."""
+    rng = np.random.Generator(np.random.PCG64(s.seed + 104729))
+    shape = (n_layers, s.L_d, s.hkv, s.d)
+    cached = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(s.cache_std)
+    scale = (np.exp(rng.standard_normal(size=(1, s.L_d, 1, 1)) * 0.5) * 0.1).astype(np.float32)
+    fresh = cached + rng.standard_normal(size=shape, dtype=np.float32) * scale
+    if s.dtype == BF16:
+        return f32_to_bf16_bits(fresh), f32_to_bf16_bits(cached)
+    return fresh, cached
+
+
 @dataclass
 class Batch:
     """Requests concatenated along the token axis, with prefix offsets.

@@ -19,15 +19,21 @@ the order the paper gives (Sec. 2):
   4. state fusion: stage outputs written into the hidden-state rows of their
      tokens (Sec. 2 item 3).
 
-For the comparison with the schemes the Complexity Analysis contrasts DAF
-with, it also gives full recomputation (causal attention over every token) and
+The step before the path, important-token selection (Sec. 2 item 1), is given
+as a score per document token (KV deviation averaged over the selection
+layers) and a top-n choice returned in original order. For the comparison with
+the schemes the Complexity Analysis contrasts DAF with, it also gives full recomputation (causal attention over every token) and
 the CacheBlend pattern (important and question tokens over the full context,
 causal by original position).
 
 Arrays are numpy. Raw buffers (bf16 bit patterns as uint16, or float32) are
 moved byte for byte; attention inputs are float32 and outputs are float64.
 Parity is pinned by the CPU test suite (closed forms, library reductions,
-invariants and planted mistakes); no function here is "parity unpinned".
+invariants and planted mistakes). One reading has nothing in the paper to pin
+it to: the selection score's norm and its aggregation over layers (the paper
+names the signal, KV deviation over the 2nd to 4th layers, but gives no
+formula), so for ``selection_scores`` the pins check the implementation of that
+reading and its parity against the paper is unpinned.
 """
 from __future__ import annotations
 
@@ -228,6 +234,35 @@ class Oracle:
         q = np.concatenate([np.asarray(q_imp, np.float32), np.asarray(q_q, np.float32)], axis=0)
         qpos = np.concatenate([idx, L_d + np.arange(L_q, dtype=np.int64)])
         return self.position_attention(q, k_hyb, v_hyb, qpos, scale, rows)
+
+    # ---- important-token selection (Sec. 2 item 1) -----------------------------
+    def selection_scores(self, k_fresh, k_cached) -> np.ndarray:
+        """Per document token, the mean over the selection layers of the L2
+        norm of the deviation between the freshly computed keys and the
+        offline cached keys (all KV heads and features of the token).
+
+        k_fresh, k_cached: [layers, L_d, hkv, d] float32 values. Returns
+        float64 [L_d]. The paper names the signal (KV deviation, aggregated
+        over several early layers, typically the 2nd to the 4th) but not the
+        norm or the aggregation; this is the reading the repository takes."""
+        kf = np.asarray(k_fresh, np.float64)
+        kc = np.asarray(k_cached, np.float64)
+        assert kf.shape == kc.shape and kf.ndim == 4
+        dev = (kf - kc).reshape(kf.shape[0], kf.shape[1], -1)
+        norms = np.sqrt((dev * dev).sum(axis=2))
+        if self.plant == "select_one_layer":
+            return norms[0]
+        return norms.mean(axis=0)
+
+    def select_important(self, scores, n: int) -> np.ndarray:
+        """The n tokens with the highest scores (equal scores: lower index
+        first), returned in ascending original order (the condensed sequence
+        keeps the original order)."""
+        scores = np.asarray(scores, np.float64)
+        assert 0 <= n <= len(scores)
+        ties = -np.arange(len(scores)) if self.plant == "select_tie_high" else np.arange(len(scores))
+        order = np.lexsort((ties, -scores))  # score desc, then index asc
+        return np.sort(order[:n]).astype(np.int64)
 
     def fuse_hidden(self, hidden, idx, o_imp, o_q, L_d: int):
         """State fusion (Sec. 2 item 3): hidden[idx[i]] = o_imp[i] and

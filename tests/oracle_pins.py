@@ -393,10 +393,62 @@ def pin_position_zero_queries(orc):
             _close(lse[i, h], math.log(p + 1), what="position lse")
 
 
+def pin_selection_brute_force(orc):
+    """Selection on a tiny case, against scores written out with plain loops
+    and a choice by exhaustive comparison: token t is chosen iff fewer than n
+    tokens beat it (higher score, or equal score and lower index)."""
+    rng = _rng(51)
+    layers, L, hkv, d = 3, 9, 2, 3
+    kc = _randn(rng, layers, L, hkv, d)
+    kf = kc + _randn(rng, layers, L, hkv, d) * rng.uniform(0.1, 2.0, size=(1, L, 1, 1)).astype(np.float32)
+    sc = orc.selection_scores(kf, kc)
+    for t in range(L):
+        per_layer = []
+        for l in range(layers):
+            acc = 0.0
+            for h in range(hkv):
+                for j in range(d):
+                    diff = float(kf[l, t, h, j]) - float(kc[l, t, h, j])
+                    acc += diff * diff
+            per_layer.append(math.sqrt(acc))
+        _close(sc[t], sum(per_layer) / layers, what="score by loops")
+    for n in range(L + 1):
+        got = orc.select_important(sc, n)
+        want = [t for t in range(L)
+                if sum(1 for u in range(L) if sc[u] > sc[t] or (sc[u] == sc[t] and u < t)) < n]
+        assert list(got) == want, f"selection n={n}: {list(got)} vs {want}"
+
+
+def pin_selection_invariants(orc):
+    """Scaling every deviation by a constant keeps the choice; a token whose
+    keys match the cache in every layer is never chosen while tokens with a
+    deviation remain; a token deviating in a single layer counts a third as
+    much as the same deviation in all three (the layers are averaged); ties
+    go to the lower index."""
+    rng = _rng(52)
+    layers, L, hkv, d = 3, 40, 2, 8
+    kc = _randn(rng, layers, L, hkv, d)
+    dev = _randn(rng, layers, L, hkv, d) * rng.uniform(0.1, 3.0, size=(1, L, 1, 1)).astype(np.float32)
+    dev[:, 7] = 0.0
+    s1 = orc.selection_scores(kc + dev, kc)
+    s2 = orc.selection_scores(kc + 2 * dev, kc)
+    for n in (1, 10, 39):
+        assert list(orc.select_important(s1, n)) == list(orc.select_important(s2, n)), "scale"
+        assert 7 not in orc.select_important(s1, n), "zero deviation chosen"
+    one = np.zeros((layers, 2, 1, 4), np.float32)
+    base = np.zeros_like(one)
+    one[0, 0, 0, 0] = 3.0            # token 0: deviation 3 in one layer
+    one[:, 1, 0, 0] = 1.0            # token 1: deviation 1 in every layer
+    s = orc.selection_scores(one, base)
+    _close(s, [1.0, 1.0], what="layer mean")
+    assert list(orc.select_important(s, 1)) == [0], "tie to the lower index"
+
+
 ALL_PINS = [
     pin_hand_two_tokens, pin_stage1_full_recompute, pin_stage1_condensed,
     pin_stage1_position_order, pin_hybrid_cache, pin_stage2_concat, pin_constant_values,
     pin_zero_queries, pin_gqa_groups, pin_needle, pin_probabilities, pin_layer_independence,
     pin_layer_full_recompute, pin_gather_scatter, pin_fuse_rows, pin_brute_force_subsets,
     pin_full_recompute_patterns, pin_cacheblend_rows, pin_position_zero_queries,
+    pin_selection_brute_force, pin_selection_invariants,
 ]

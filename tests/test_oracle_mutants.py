@@ -7,7 +7,8 @@ term dropped from the softmax sum, a lost gather row, reversed scatter sources,
 the question's own key dropped, a feature dropped from the dot product, a
 position mask one key too wide). The
 Python plants skip the hybrid write-back, leave the question K/V out of the
-cache, or fuse question rows one row early.
+cache, fuse question rows one row early, score selection from one layer only,
+or break selection ties toward the higher index.
 """
 import os
 
@@ -18,7 +19,7 @@ from oracle import build as orc_build
 from oracle_pins import ALL_PINS
 
 C_MUTANTS = list(range(1, 13))
-PY_PLANTS = ["no_hybrid", "no_question_kv", "fuse_shift"]
+PY_PLANTS = ["no_hybrid", "no_question_kv", "fuse_shift", "select_one_layer", "select_tie_high"]
 
 
 def _failures(orc):
