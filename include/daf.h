@@ -122,6 +122,26 @@ daf_status_t daf_gather_important(const daf_batch_t *batch, int32_t src_layout,
                                   const int32_t *idx, void *dst,
                                   hipStream_t stream);
 
+/* Important-token selection, the step before the path (Sec. 2 item 1: tokens
+ * are chosen by the deviation of their recomputed KV from the offline cache,
+ * aggregated over several early layers, typically the 2nd to the 4th).
+ *   k_fresh[l], k_cached[l], l < n_layers (1..8): a HOST array of DEVICE
+ *   pointers per argument; each tensor is [sum L_d][Hkv][D] of `dtype`,
+ *   request b's document rows from cu_doc[b] (documents only), 16-byte aligned.
+ *   scores (DEVICE float32 [sum L_d], output): per document token, the mean
+ *   over the layers of the L2 norm of k_fresh - k_cached over its Hkv*D values
+ *   (the paper names the signal but not the norm or the aggregation).
+ *   idx (DEVICE int32 [sum n], output): for request b, the n_b = cu_imp[b+1] -
+ *   cu_imp[b] tokens with the highest scores (equal scores: lower index
+ *   first), request-local, strictly increasing - the idx the other entry
+ *   points take.
+ * Hkv * D * element size must not exceed 4096 bytes (DAF_ERR_UNSUPPORTED). */
+daf_status_t daf_select_important(const daf_attn_cfg_t *cfg,
+                                  const daf_batch_t *batch, int32_t n_layers,
+                                  const void *const *k_fresh,
+                                  const void *const *k_cached, float *scores,
+                                  int32_t *idx, hipStream_t stream);
+
 /* Stage 1, important-token self-attention (Sec. 2 item 1; Complexity
  * Analysis: important tokens attend only to each other, O(r^2 L_d^2)).
  *   q_imp [sum n][Hq][D], k_imp / v_imp [sum n][Hkv][D] -> o_imp [sum n][Hq][D]

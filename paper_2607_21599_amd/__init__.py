@@ -17,7 +17,7 @@ __all__ = [
     "DAF_OK", "DAF_BF16", "DAF_F32", "DAF_SRC_TOKENS", "DAF_SRC_DOCS", "DAF_FUSE_KV",
     "DAF_FUSE_HIDDEN", "DafError", "AttnCfg", "Batch", "lib", "library_path",
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
-    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices",
+    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
     "daf_status_string", "daf_last_error", "daf_version", "EXPORTED",
 ]
 
@@ -30,7 +30,7 @@ DAF_FUSE_KV, DAF_FUSE_HIDDEN = 1, 2
 # every symbol include/daf.h declares
 EXPORTED = [
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
-    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices",
+    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
     "daf_status_string", "daf_last_error", "daf_version",
 ]
 
@@ -94,6 +94,7 @@ def lib() -> ctypes.CDLL:
             "daf_imp_self_attn": (i32, [cfgp, bp, _vp, _vp, _vp, _vp, _vp, _vp]),
             "daf_position_attn": (i32, [cfgp, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, _vp,
                                         _vp]),
+            "daf_select_important": (i32, [cfgp, bp, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp]),
             "daf_qdoc_workspace_size": (sz, [cfgp, bp]),
             "daf_qdoc_attn": (i32, [cfgp, bp, _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp]),
             "daf_fuse": (i32, [cfgp, bp, u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -164,6 +165,17 @@ def daf_imp_self_attn(cfg: AttnCfg, batch: Batch, q_imp, k_imp, v_imp, o_imp, ls
 def daf_position_attn(cfg: AttnCfg, n_rows: int, n_keys: int, q, q_pos, k, v, o, lse=None, stream=None):
     _check(lib().daf_position_attn(_cfgp(cfg), n_rows, n_keys, _ptr(q), _ptr(q_pos), _ptr(k), _ptr(v),
                                    _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def daf_select_important(cfg: AttnCfg, batch: Batch, k_fresh, k_cached, scores, idx, stream=None):
+    """k_fresh / k_cached: sequences (one entry per selection layer) of device
+    tensors or addresses, passed as host arrays of device pointers."""
+    nl = len(k_fresh)
+    fresh = (ctypes.c_void_p * max(nl, 1))(*[_ptr(t) for t in k_fresh])
+    cached = (ctypes.c_void_p * max(len(k_cached), 1))(*[_ptr(t) for t in k_cached])
+    _check(lib().daf_select_important(_cfgp(cfg), _bp(batch), nl, ctypes.cast(fresh, ctypes.c_void_p),
+                                      ctypes.cast(cached, ctypes.c_void_p), _ptr(scores), _ptr(idx),
+                                      _stream(stream)))
 
 
 def daf_qdoc_workspace_size(cfg: AttnCfg, batch: Batch) -> int:

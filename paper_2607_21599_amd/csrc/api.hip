@@ -512,6 +512,59 @@ daf_status_t daf_position_attn(const daf_attn_cfg_t *cfg, int32_t n_rows, int32_
   }
 }
 
+daf_status_t daf_select_important(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, int32_t n_layers,
+                                  const void *const *k_fresh, const void *const *k_cached, float *scores,
+                                  int32_t *idx, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    if (n_layers < 1 || n_layers > kMaxSelectLayers)
+      return fail(DAF_ERR_INVALID_ARG, "n_layers=%d (supported: 1..%d)", n_layers, kMaxSelectLayers);
+    const int64_t row_bytes = (int64_t)c.hkv * c.d * c.elem;
+    if (row_bytes > 4096)
+      return fail(DAF_ERR_UNSUPPORTED, "Hkv*D*element = %lld bytes per token exceeds 4096", (long long)row_bytes);
+    const int64_t rows = b.total_tok - b.total_q;  // document rows
+    if (rows == 0) return ok();
+    if (!k_fresh || !k_cached) return fail(DAF_ERR_INVALID_ARG, "k_fresh and k_cached must be non-NULL host arrays");
+    SelectLaunch p{};
+    for (int l = 0; l < n_layers; ++l) {
+      CHECK(need_ptr(k_fresh[l], "k_fresh[l]"));
+      CHECK(need_ptr(k_cached[l], "k_cached[l]"));
+      p.fresh[l] = k_fresh[l];
+      p.cached[l] = k_cached[l];
+    }
+    CHECK(need_ptr(scores, "scores"));
+    if (b.total_imp > 0) CHECK(need_ptr(idx, "idx"));
+    p.scores = scores;
+    p.idx = idx;
+    p.rows = rows;
+    p.row_bytes = (int32_t)row_bytes;
+    p.n_layers = n_layers;
+    hipError_t e = launch_select_scores(p, c.dtype == DAF_BF16, stream);
+    if (e != hipSuccess) return hip_fail(e, "selection score launch");
+    int64_t doc0 = 0;
+    for (size_t i = 0; i < b.r.size(); ++i) {
+      const Req &q = b.r[i];
+      if (q.n > 0) {
+        p.req[p.n_req++] = SelectReq{doc0, q.L_d, q.n, q.imp0};
+        if (p.n_req == kMaxSelectReqs) {
+          e = launch_select_topn(p, stream);
+          if (e != hipSuccess) return hip_fail(e, "selection launch");
+          p.n_req = 0;
+        }
+      }
+      doc0 += q.L_d;
+    }
+    e = launch_select_topn(p, stream);
+    if (e != hipSuccess) return hip_fail(e, "selection launch");
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
 size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg, const daf_batch_t *batch) {
   try {
     Cfg c;

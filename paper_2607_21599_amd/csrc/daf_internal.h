@@ -84,6 +84,29 @@ struct MergeLaunch {
   MergeEntry e[kMaxEntries];
 };
 
+// Important-token selection: per-row scores over the selection layers, then a
+// top-n per request (up to kMaxSelectReqs requests per top-n launch).
+constexpr int kMaxSelectLayers = 8;
+constexpr int kMaxSelectReqs = 64;
+struct SelectReq {
+  int64_t doc0;   // first score (document row) of the request
+  int32_t L_d;    // document rows
+  int32_t n;      // tokens to keep
+  int32_t imp0;   // first output index slot (cu_imp[b])
+};
+struct SelectLaunch {
+  const void *fresh[kMaxSelectLayers];   // [rows][Hkv][D] per layer
+  const void *cached[kMaxSelectLayers];
+  float *scores;                         // [rows]
+  int32_t *idx;                          // [sum n]
+  int64_t rows;
+  int32_t row_bytes;                     // Hkv * D * element bytes, multiple of 16, <= 4096
+  int32_t n_layers;
+  int32_t n_req;
+  SelectReq req[kMaxSelectReqs];
+};
+static_assert(sizeof(SelectLaunch) < 4096, "selection launch must fit 4 KiB of kernel arguments");
+
 // Row movement (gather / scatter), byte copies in 16-byte units.
 struct RowReq {
   int64_t base;     // token-row base of the request in the full-length buffer
@@ -124,5 +147,7 @@ hipError_t launch_scatter(const RowLaunch &p, const ScatterPair *pairs,
                           int n_pairs, hipStream_t s);
 hipError_t launch_check_indices(const RowLaunch &p, int32_t *d_bad,
                                 int accumulate, hipStream_t s);
+hipError_t launch_select_scores(const SelectLaunch &p, bool bf16, hipStream_t st);
+hipError_t launch_select_topn(const SelectLaunch &p, hipStream_t st);
 
 }  // namespace daf

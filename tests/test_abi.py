@@ -141,3 +141,25 @@ def test_position_attn_checks():
         daf.daf_position_attn(c, 3, 1 << 22, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
     assert e.value.status == daf.DAF_ERR_UNSUPPORTED
     daf.daf_position_attn(c, 0, 10, None, None, None, None, None, None, 0)  # no rows: no-op
+
+
+def test_select_important_checks():
+    c = _cfg()
+    b = daf.Batch.single(100, 8, 10)
+    with pytest.raises(daf.DafError) as e:  # no layers
+        daf.daf_select_important(c, b, [], [], FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # more than 8 layers
+        daf.daf_select_important(c, b, [FAKE] * 9, [FAKE] * 9, FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_select_important(c, b, [FAKE, FAKE + 4], [FAKE, FAKE], FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_ALIGNMENT
+    with pytest.raises(daf.DafError) as e:
+        daf.daf_select_important(c, b, [FAKE], [FAKE], None, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # token rows wider than 4 KiB
+        daf.daf_select_important(_cfg(n_q_heads=32, n_kv_heads=16, dtype=daf.DAF_F32), b, [FAKE], [FAKE],
+                                 FAKE, FAKE, 0)
+    assert e.value.status == daf.DAF_ERR_UNSUPPORTED
+    daf.daf_select_important(c, daf.Batch.single(0, 3, 0), [FAKE], [FAKE], None, None, 0)  # no documents
