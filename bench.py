@@ -259,6 +259,45 @@ def main():
                     traffic=measured_traffic(args.workload), traffic_unit="bytes per launch (HBM, counters)",
                     flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
 
+    selection = None
+    if not args.no_patterns:
+        # The step before the path: choosing the important tokens from the KV
+        # deviation over three selection layers (same spin + event timing).
+        print("[bench] important-token selection", file=sys.stderr, flush=True)
+        import paper_2607_21599_amd as daf_mod
+        from paper_2607_21599_amd.tensors import to_device
+        n_sel_layers = 3
+        pairs = [di.make_selection_inputs(s, n_sel_layers) for s in shapes]
+        fresh = [to_device(np.ascontiguousarray(np.concatenate([p[0][l] for p in pairs])))
+                 for l in range(n_sel_layers)]
+        cached = [to_device(np.ascontiguousarray(np.concatenate([p[1][l] for p in pairs])))
+                  for l in range(n_sel_layers)]
+        del pairs
+        n_doc = int(batch.cu_doc[-1])
+        sel_scores = torch.empty(n_doc, dtype=torch.float32, device="cuda")
+        sel_idx = torch.empty(int(batch.cu_imp[-1]), dtype=torch.int32, device="cuda")
+        b0 = bufs[0]
+
+        def run_sel():
+            daf_mod.daf_select_important(b0.cfg, b0.batch, fresh, cached, sel_scores, sel_idx)
+
+        run_sel()
+        torch.cuda.synchronize()
+        reps = 10
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for i in range(reps):
+            torch.cuda._sleep(spin_cycles)
+            ev[i][0].record()
+            run_sel()
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        sel_us = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        eb = 2 if s0.dtype == di.BF16 else 4
+        sel_bytes = 2 * n_sel_layers * n_doc * s0.hkv * s0.d * eb + 4 * n_doc + 4 * int(batch.cu_imp[-1])
+        selection = {"us": sel_us, "layers": n_sel_layers, "bytes": sel_bytes, "GBps": gbs(sel_bytes, sel_us),
+                     "hbm_frac": gbs(sel_bytes, sel_us) / PEAK_HBM_GBS}
+        del fresh, cached
+
     comparison = None
     if not args.no_patterns and len(shapes) == 1:
         # The schemes the Complexity Analysis compares DAF with, as attention on
@@ -312,6 +351,8 @@ def main():
         "stages": stages,
         "roofline": roofline,
     }
+    if selection is not None:
+        out["selection"] = selection
     if comparison is not None:
         out["comparison"] = comparison
     if not args.no_cpu_baseline:

@@ -10,13 +10,16 @@
 // bytes read per row); every lane loads 16-byte pieces of the row for all
 // layers before reducing, fp32 sums of squares, a wave reduction per layer.
 //
-// select_topn_kernel: one 1024-thread workgroup per request. Scores are
+// select_topn_kernel: one 1024-thread workgroup per request, the keys held in
+// registers (32 per lane, slab by slab beyond 32k tokens). Scores are
 // non-negative floats, so their bit patterns order like the values: a radix
-// select over four 8-bit digits (histograms in LDS) finds the key T of the
-// n-th highest score and how many tokens scoring exactly T to keep; one pass
-// in index order then keeps every token above T and the first of those equal
-// to T, placing each kept index with a block-wide prefix count, so the output
-// comes out sorted.
+// select over 8-bit digits finds the key T of the n-th highest score and how
+// many tokens scoring exactly T to keep. The passes start below the bits that
+// the lowest and highest key share, so the first histogram spreads over the
+// scores' actual range, and stop early once a digit's keys are all taken.
+// Each wave owns a contiguous range of tokens; a prefix sum over the waves of
+// their kept counts, then ballots within each wave, place every kept index, so
+// the output comes out sorted.
 #include "daf_internal.h"
 
 namespace daf {
@@ -97,84 +100,174 @@ __global__ __launch_bounds__(kScoreThreads) void select_score_kernel(const Selec
   if (lane == 0) p.scores[row] = acc / (float)p.n_layers;
 }
 
-// Block-wide exclusive prefix count of `flag` in thread order; returns this
-// thread's prefix and sets `total`. Uses `wsum` (kTopnWaves ints of LDS).
-__device__ __forceinline__ int block_prefix(bool flag, int *wsum, int &total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const unsigned long long bal = __builtin_amdgcn_ballot_w64(flag);
-  const unsigned long long below = lane ? (bal & ((1ull << lane) - 1ull)) : 0ull;
-  const int in_wave = __popcll(below);
-  if (lane == 0) wsum[wave] = __popcll(bal);
+// Requests up to kSlabKeys tokens are held in registers whole (32 keys per
+// lane); longer ones are streamed through 16k-token slabs, reloaded per pass.
+constexpr int kSlabKeys = kTopnThreads * 32;
+
+// Exclusive prefix sum over the waves of a wave-uniform value, in wave order;
+// also returns the sum over all waves. wsum: kTopnWaves ints of LDS.
+__device__ __forceinline__ int wave_scan(int v, int *wsum, int &total) {
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) wsum[wave] = v;
   __syncthreads();
   int before = 0;
   total = 0;
 #pragma unroll
   for (int w = 0; w < kTopnWaves; ++w) {
-    const int v = wsum[w];
-    before += w < wave ? v : 0;
-    total += v;
+    const int t = wsum[w];
+    before += w < wave ? t : 0;
+    total += t;
   }
   __syncthreads();  // wsum is reused by the next call
-  return before + in_wave;
+  return before;
 }
 
+// Exclusive prefix sum of v over the threads in thread order.
+__device__ __forceinline__ int block_scan(int v, int *wsum) {
+  const int lane = threadIdx.x & 63;
+  int inc = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(inc, off, 64);
+    if (lane >= off) inc += t;
+  }
+  int total;
+  const int before = wave_scan(__shfl(inc, 63, 64), wsum, total);
+  return before + inc - v;
+}
+
+// Number of set bits of m below this lane.
+__device__ __forceinline__ int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
+__device__ __forceinline__ unsigned long long ballot(bool x) { return __builtin_amdgcn_ballot_w64(x); }
+
+// KPL keys per lane; MULTI: a request may span more than one slab.
+template <int KPL, bool MULTI>
 __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectLaunch p) {
+  constexpr int kSlab = kTopnThreads * KPL, kWaveSlab = kSlab / kTopnWaves;
   __shared__ int hist[256];
   __shared__ int wsum[kTopnWaves];
-  __shared__ unsigned s_prefix;
-  __shared__ int s_remaining;
+  __shared__ unsigned s_lo[kTopnWaves], s_hi[kTopnWaves], s_prefix;
+  __shared__ int s_remaining, s_top;
   const int b = blockIdx.x;
   const int L = p.req[b].L_d, n = p.req[b].n;
   if (n <= 0 || L <= 0) return;
   const unsigned *key = reinterpret_cast<const unsigned *>(p.scores + p.req[b].doc0);
   int32_t *out = p.idx + p.req[b].imp0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n_slabs = MULTI ? (L + kSlab - 1) / kSlab : 1;
 
-  // ---- radix select: key T of the n-th highest score -------------------------
-  unsigned prefix = 0u, mask = 0u;
-  int remaining = n;  // how many still to take among keys matching the prefix
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = threadIdx.x; i < 256; i += kTopnThreads) hist[i] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < L; i += kTopnThreads) {
-      const unsigned k = key[i];
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+  // slab s: wave w owns keys s*kSlab + w*kWaveSlab + [0, kWaveSlab); its lane
+  // holds key j*64 + lane of that range in k[j]
+  unsigned k[KPL];
+  int slab_base = 0;  // first key of the wave's range in the loaded slab
+  int lane_end = 0;   // key j of this lane is a token when j * 64 < lane_end
+  auto load = [&](int s) {
+    slab_base = s * kSlab + wave * kWaveSlab;
+    lane_end = L - slab_base - lane;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const int i = slab_base + j * 64 + lane;
+      k[j] = i < L ? key[i] : 0u;
+    }
+  };
+  auto valid = [&](int j) { return j * 64 < lane_end; };
+
+  // ---- bits common to every key: the radix passes start below them ----------
+  unsigned lo = 0xffffffffu, hi = 0u;
+  for (int s = 0; s < n_slabs; ++s) {
+    load(s);
+#pragma unroll
+    for (int j = 0; j < KPL; ++j)
+      if (valid(j)) {
+        lo = min(lo, k[j]);
+        hi = max(hi, k[j]);
+      }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = min(lo, (unsigned)__shfl_xor((int)lo, off, 64));
+    hi = max(hi, (unsigned)__shfl_xor((int)hi, off, 64));
+  }
+  if (lane == 0) {
+    s_lo[wave] = lo;
+    s_hi[wave] = hi;
+  }
+  if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kTopnWaves; ++w) {
+    lo = min(lo, s_lo[w]);
+    hi = max(hi, s_hi[w]);
+  }
+  // undecided low bits: keys agree on every bit at or above `top`
+  int top = lo == hi ? 0 : 32 - __builtin_clz(lo ^ hi);
+  unsigned prefix = lo & (top == 32 ? 0u : ~((1u << top) - 1u));
+  int remaining = n;  // keys still to take among those matching prefix above `top`
+
+  // ---- radix select of the n-th highest key, 8 bits per pass -----------------
+  while (top > 0) {
+    const int w = min(8, top), shift = top - w;
+    const unsigned decided = top == 32 ? 0u : ~0u << top;  // bits matched against prefix
+    for (int s = 0; s < n_slabs; ++s) {
+      if (MULTI) load(s);
+#pragma unroll
+      for (int j = 0; j < KPL; ++j)
+        if (valid(j) && ((k[j] ^ prefix) & decided) == 0u)
+          atomicAdd(&hist[(k[j] >> shift) & ((1u << w) - 1u)], 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int cum = 0, dsel = 0;
-      for (int d = 255; d >= 0; --d) {
-        if (cum + hist[d] >= remaining) {
-          dsel = d;
-          break;
-        }
-        cum += hist[d];
-      }
-      s_prefix = prefix | ((unsigned)dsel << shift);
-      s_remaining = remaining - cum;
+    // digits from the highest down: the selected one holds the remaining-th key
+    if (threadIdx.x == 0) s_top = 0;  // every pass ends the loop unless a digit is chosen
+    const int d = (1 << w) - 1 - (int)threadIdx.x;
+    int h = 0;
+    if (d >= 0) {
+      h = hist[d];
+      hist[d] = 0;  // cleared for the next pass
+    }
+    const int above = block_scan(h, wsum);
+    if (d >= 0 && above < remaining && above + h >= remaining) {
+      s_prefix = prefix | ((unsigned)d << shift);
+      // every key in the digit is taken: no lower bits need deciding
+      s_top = above + h == remaining ? 0 : shift;
+      s_remaining = above + h == remaining ? 0x7fffffff : remaining - above;
     }
     __syncthreads();
     prefix = s_prefix;
+    top = s_top;
     remaining = s_remaining;
-    mask |= 255u << shift;
-    __syncthreads();
   }
-  const unsigned T = prefix;  // tokens above T are all kept, `remaining` of those equal to T
+  const unsigned T = prefix;  // keep keys above T and the first `remaining` equal to T
 
-  // ---- keep in index order -------------------------------------------------
-  int kept = 0, ties = 0;
-  for (int base = 0; base < L; base += kTopnThreads) {
-    const int i = base + threadIdx.x;
-    const unsigned k = i < L ? key[i] : 0u;
-    const bool gt = i < L && k > T;
-    const bool eq = i < L && k == T;
-    int n_eq;
-    const int tie_rank = ties + block_prefix(eq, wsum, n_eq);
-    const bool sel = gt || (eq && tie_rank < remaining);
-    int n_sel;
-    const int pos = kept + block_prefix(sel, wsum, n_sel);
-    if (sel) out[pos] = i;
-    kept += n_sel;
-    ties += n_eq;
+  // ---- ordered compaction, slab by slab --------------------------------------
+  int out_base = 0, eq_base = 0;  // kept and equal-to-T keys of earlier slabs
+  for (int s = 0; s < n_slabs; ++s) {
+    if (MULTI) load(s);
+    int n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      n_gt += __popcll(ballot(valid(j) && k[j] > T));
+      n_eq += __popcll(ballot(valid(j) && k[j] == T));
+    }
+    int eq_total, kept_total;
+    const int eq_before = eq_base + wave_scan(n_eq, wsum, eq_total);
+    const int eq_keep = max(0, min(n_eq, remaining - eq_before));
+    int pos = out_base + wave_scan(n_gt + eq_keep, wsum, kept_total);
+    int eq_seen = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const bool v = valid(j);
+      const unsigned long long eq = ballot(v && k[j] == T);
+      const bool keep = (v && k[j] > T) || ((eq >> lane & 1ull) && eq_seen + lanes_below(eq) < eq_keep);
+      const unsigned long long km = ballot(keep);
+      if (keep) out[pos + lanes_below(km)] = slab_base + j * 64 + lane;
+      pos += __popcll(km);
+      eq_seen += __popcll(eq);
+    }
+    out_base += kept_total;
+    eq_base += eq_total;
   }
 }
 
@@ -199,7 +292,10 @@ hipError_t launch_select_scores(const SelectLaunch &p, bool bf16, hipStream_t st
 
 hipError_t launch_select_topn(const SelectLaunch &p, hipStream_t st) {
   if (p.n_req <= 0) return hipSuccess;
-  select_topn_kernel<<<p.n_req, kTopnThreads, 0, st>>>(p);
+  int longest = 0;
+  for (int b = 0; b < p.n_req; ++b) longest = std::max(longest, p.req[b].L_d);
+  if (longest > kSlabKeys) select_topn_kernel<16, true><<<p.n_req, kTopnThreads, 0, st>>>(p);
+  else select_topn_kernel<32, false><<<p.n_req, kTopnThreads, 0, st>>>(p);
   return hipGetLastError();
 }
 

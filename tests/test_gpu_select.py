@@ -98,3 +98,41 @@ def test_select_all_and_ties(n_layers):
         if n >= 400:
             zeros = np.setdiff1d(np.arange(sh.L_d), dev_rows)[: n - 400]
             assert np.array_equal(got, np.union1d(dev_rows, zeros)), f"n={n}: ties not to the lowest indices"
+
+
+def test_select_long_request_ties_across_slabs():
+    """A request longer than the keys one workgroup holds in registers (a
+    40000-token document beside a 5000-token one): only 300 tokens deviate,
+    so the kept zero-score ties run across slab boundaries in index order."""
+    rng = np.random.Generator(np.random.PCG64(11))
+    shs, fresh_l, cached_l = [], [], []
+    for L, n in ((40000, 20000), (5000, 900)):
+        s = di.Shape("sel_long", L_d=L, L_q=3, n=n, hq=2, hkv=1, d=64, seed=91 + L)
+        f, c = di.make_selection_inputs(s, 1)
+        dev = np.sort(rng.choice(L, size=300, replace=False))
+        keep = np.zeros(L, bool)
+        keep[dev] = True
+        fresh_l.append(np.where(keep[None, :, None, None], f, c))
+        cached_l.append(c)
+        shs.append((s, dev))
+    for n0 in (20000, 39000, 300, 1):
+        sh = [di.Shape("sel_long", L_d=40000, L_q=3, n=n0, hq=2, hkv=1, d=64, seed=1), shs[1][0]]
+        cu_imp = np.array([0, n0, n0 + sh[1].n])
+        batch = di.Batch(sh, {}, np.array([0, 40000, 45000]), np.array([0, 3, 6]), cu_imp)
+        scores, idx = _run(batch, fresh_l, cached_l, 1)
+        _check(batch, fresh_l, cached_l, scores, idx)
+        got = idx[:n0]
+        dev = shs[0][1]
+        want = np.union1d(dev, np.setdiff1d(np.arange(40000), dev)[: n0 - 300]) if n0 >= 300 else None
+        if want is not None:
+            assert np.array_equal(got, want), f"n={n0}: ties across slabs not to the lowest indices"
+
+
+def test_select_all_scores_equal():
+    """No token deviates: every score is 0 and the first n tokens are kept."""
+    s = di.Shape("sel_flat", L_d=2500, L_q=2, n=123, hq=2, hkv=1, d=64, seed=5)
+    _, c = di.make_selection_inputs(s, 2)
+    batch = di.Batch([s], {}, np.array([0, s.L_d]), np.array([0, 2]), np.array([0, s.n]))
+    scores, idx = _run(batch, [c.copy()], [c], 2)
+    assert np.all(scores == 0.0)
+    assert np.array_equal(idx[: s.n], np.arange(s.n))
