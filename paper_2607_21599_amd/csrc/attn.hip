@@ -320,37 +320,42 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
   }
 }
 
-// Log-sum-exp merge of the key splits. D/4 threads per (query row, head), each
-// owning 4 features: m = max_s lse_s, w_s = exp(lse_s - m), O = sum_s w_s O_s /
-// sum_s w_s, lse = m + log sum_s w_s. Split partials are read with 16-byte
-// loads, several splits in flight per thread.
+// Log-sum-exp merge of the key splits. Each (query row, head) item gets two
+// groups of D/4 threads, each thread owning 4 features; group j merges its
+// half of the splits (m = max_s lse_s, w_s = exp(lse_s - m), acc = sum_s w_s
+// O_s, wsum = sum_s w_s), then the two halves are combined across the lanes
+// (lane ^ D/4) and the first group writes O = acc / wsum and lse = m + log
+// wsum. Split partials are read with 16-byte loads, all of a half's splits in
+// flight at once for up to 32 splits (one round trip to memory).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
-  constexpr int TPI = D / 4;             // threads per (row, head) item
-  constexpr int IPB = 256 / TPI;         // items per block
-  const int item = blockIdx.x * IPB + threadIdx.x / TPI;
+  constexpr int TPI = D / 4;              // threads per item and split half
+  constexpr int IPB = 256 / (2 * TPI);    // items per block
+  const int item = blockIdx.x * IPB + threadIdx.x / (2 * TPI);
+  const int hs = (threadIdx.x / TPI) & 1;  // which half of the splits
   const int t = threadIdx.x % TPI;
   const int row = item / p.hq, h = item % p.hq;
-  if (row >= p.total_rows) return;
+  if (row >= p.total_rows) return;  // both halves of an item leave together
   int ei = 0;
   while (ei + 1 < p.n_entries && p.e[ei + 1].row0 <= row) ++ei;
   const MergeEntry &E = p.e[ei];
   const int r = row - E.row0;
   const int S = E.n_splits;
+  const int per_half = (S + 1) / 2;
+  const int sb = hs * per_half, se = min(S, sb + per_half);
   const size_t prow0 = (size_t)r * S;
   const float *lse = E.part_lse + prow0 * p.hq + h;
   const float *src = E.part_o + (prow0 * p.hq + h) * D + 4 * t;
   const size_t split_stride = (size_t)p.hq * D;
-  // the loads of up to U splits go out before any of them is used
   constexpr int U = 16;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, wsum = 0.f;
-  for (int s0 = 0; s0 < S; s0 += U) {
+  for (int s0 = sb; s0 < se; s0 += U) {
     float ls[U];
     f32x4 po[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (s0 + u < S) {
+      if (s0 + u < se) {
         ls[u] = lse[(size_t)(s0 + u) * p.hq];
         po[u] = *reinterpret_cast<const f32x4 *>(src + (s0 + u) * split_stride);
       } else {
@@ -373,6 +378,20 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
       acc += w * po[u];
     }
   }
+  // combine with the other half
+  {
+    const float m2 = __shfl_xor(m, TPI, 64), w2 = __shfl_xor(wsum, TPI, 64);
+    f32x4 acc2;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc2[j] = __shfl_xor(acc[j], TPI, 64);
+    const float mm = fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : __expf(m - mm);
+    const float b = (m2 == -INFINITY) ? 0.f : __expf(m2 - mm);
+    wsum = wsum * a + w2 * b;
+    acc = acc * a + acc2 * b;
+    m = mm;
+  }
+  if (hs != 0) return;
   const float inv = 1.f / wsum;
   T *dst = static_cast<T *>(E.o) + ((size_t)r * p.hq + h) * D + 4 * t;
   typename Vec<T>::v4 o;
@@ -399,7 +418,7 @@ hipError_t launch_attn_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
 template <typename T, int D>
 hipError_t launch_merge_t(const MergeLaunch &p, hipStream_t st) {
   const int items = p.total_rows * p.hq;
-  constexpr int IPB = 256 / (D / 4);
+  constexpr int IPB = 256 / (2 * (D / 4));
   lse_merge_kernel<T, D><<<dim3((items + IPB - 1) / IPB), dim3(256), 0, st>>>(p);
   return hipGetLastError();
 }
