@@ -94,6 +94,17 @@ def work(shapes) -> dict:
                 fuse_hidden_bytes=bhid, gather_bytes=bgat)
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
     """The oracle on every stride1-th stage-1 row and every stride2-th stage-2
     row (plus the full hybrid-cache build and fusion), scaled to the layer."""
@@ -125,7 +136,7 @@ def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
         t_total += t_hyb + t_fuse + t_s1 * s.n / max(1, len(rows1)) + t_s2 * s.L_q / max(1, len(rows2))
         rows_done[0] += len(rows1)
         rows_done[1] += len(rows2)
-    return dict(value=t_total * 1e6, unit="us", cores=orc.threads, kind="oracle",
+    return dict(value=t_total * 1e6, unit="us", cores=orc.threads, kind="oracle", cpu=cpu_model(),
                 sample=(f"stage-1 rows 0::{stride1} ({rows_done[0]} rows) and stage-2 rows 0::{stride2} "
                         f"({rows_done[1]} rows) of every request, full hybrid-cache build and fusion; "
                         "attention times scaled by total/sampled rows"))
@@ -208,7 +219,7 @@ def main():
         "fuse_hidden": lambda j: bufs[j].fuse_hidden(),
     }
     spin_cycles = 400_000  # ~0.2 ms at the MI355X shader clock, longer than a host call
-    stage_us = {}
+    stage_us, stage_pct = {}, {}
     for n in names:
         calls[n](0)
         torch.cuda.synchronize()
@@ -219,7 +230,9 @@ def main():
             calls[n](i % len(bufs))
             ev[i][1].record()
         torch.cuda.synchronize()
-        stage_us[n] = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        t_us = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+        stage_us[n] = float(np.mean(t_us))
+        stage_pct[n] = [float(x) for x in np.percentile(t_us, [10, 50, 90])]
     wk = work(shapes)
     peak_mma = PEAK_BF16_TFLOPS if s0.dtype == di.BF16 else PEAK_F32_TFLOPS
 
@@ -244,6 +257,8 @@ def main():
                             GBps=gbs(wk["fuse_hidden_bytes"], stage_us["fuse_hidden"]),
                             bytes=wk["fuse_hidden_bytes"]),
     }
+    for k, n in zip(stages, names):
+        stages[k]["us_p10_p50_p90"] = stage_pct[n]
     for k in ("gather", "fuse_kv", "fuse_hidden"):
         stages[k]["hbm_frac"] = stages[k]["GBps"] / PEAK_HBM_GBS
     for k in ("stage1_imp_self_attn", "stage2_qdoc_attn"):

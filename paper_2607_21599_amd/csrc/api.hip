@@ -138,14 +138,25 @@ struct Split {
   int n_splits, split_keys;
 };
 
+// The bf16 split-key kernel packs (query head, 32-row block) units of a KV
+// group four to a workgroup; the fp32 kernel runs one head per workgroup.
+bool packed_qdoc(const Cfg &c) { return c.dtype == DAF_BF16; }
+// workgroups per KV head and key split for a question of L_q rows
+int qdoc_blocks(const Cfg &c, int L_q) {
+  if (!packed_qdoc(c)) return (L_q + kAttnBM - 1) / kAttnBM;
+  const int units = c.group * ((L_q + 31) / 32);
+  return (units + 3) / 4;
+}
+
 std::vector<Split> plan_splits(const Cfg &c, const Batch &b) {
   const int BN = c.key_tile;
   double work = 0;
   for (const Req &q : b.r) {
     if (q.L_q == 0) continue;
-    const int mbs = (q.L_q + kAttnBM - 1) / kAttnBM;
     const int kbs = (q.L_d + q.L_q + BN - 1) / BN;
-    work += (double)c.hq * mbs * kbs;
+    // workgroups per split times key tiles
+    const int wgs = packed_qdoc(c) ? c.hkv * qdoc_blocks(c, q.L_q) : c.hq * qdoc_blocks(c, q.L_q);
+    work += (double)wgs * kbs;
   }
   const double per_wg = std::max(1.0, work / kTargetWorkgroups);
   std::vector<Split> out(b.r.size());
@@ -214,7 +225,7 @@ AttnEntry qdoc_entry(const Cfg &c, const Req &q, const Split &sp, int64_t part_r
   e.part_lse = part_lse + part_row0 * c.hq;
   e.n_rows = q.L_q;
   e.n_keys = q.L_d + q.L_q;
-  const int mbs = (q.L_q + kAttnBM - 1) / kAttnBM;
+  const int mbs = qdoc_blocks(c, q.L_q);
   e.mb_hi = mbs - 1;
   e.mb_count = mbs;
   e.n_splits = sp.n_splits;
@@ -230,6 +241,7 @@ daf_status_t run_entries(const Cfg &c, AttnKind kind, std::vector<AttnEntry> &en
     p.hq = c.hq;
     p.hkv = c.hkv;
     p.group = c.group;
+    p.wgs_per_group = (kind == AttnKind::kQdoc && packed_qdoc(c)) ? 1 : c.group;
     p.scale_log2 = c.scale * 1.4426950408889634f;
     int groups = 0;
     const size_t i1 = std::min(entries.size(), i0 + kMaxEntries);

@@ -406,7 +406,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
 
 template <typename T, int D>
 hipError_t launch_attn_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
-  const int slots = p.group * ((p.n_groups + kXcds - 1) / kXcds);
+  const int slots = p.wgs_per_group * ((p.n_groups + kXcds - 1) / kXcds);
   const dim3 grid(kXcds * slots), block(kAttnThreads);
   switch (kind) {
     case AttnKind::kSelf: attn_fwd_kernel<T, D, 0><<<grid, block, 0, st>>>(p); break;

@@ -322,21 +322,21 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   // otherwise work groups are dealt to the XCDs round-robin. Within an XCD,
   // work groups run heaviest first, and the G heads of a work group are
   // consecutive workgroups of that XCD.
-  const int G = p.group;
+  const int G = p.group, WPG = p.wgs_per_group;
   const int xcd = blockIdx.x % kXcds;
   const int slot = blockIdx.x / kXcds;
-  const int hl = slot % G;
+  const int hl = slot % WPG;
   int g, lam;  // KV head, index of the work group among that head's work groups
   if (kXcds % p.hkv == 0) {
     const int xph = kXcds / p.hkv;
     g = xcd / xph;
     // work groups of a head are dealt to its xph XCDs in boustrophedon order
     // (a, b, b, a, ...), so the XCDs get equal shares of the heaviest-first list
-    const int q = slot / G, r = xcd % xph;
+    const int q = slot / WPG, r = xcd % xph;
     lam = q * xph + ((q & 1) ? xph - 1 - r : r);
     if (lam * p.hkv >= p.n_groups) return;
   } else {
-    const int gamma = (slot / G) * kXcds + xcd;
+    const int gamma = (slot / WPG) * kXcds + xcd;
     if (gamma >= p.n_groups) return;
     g = gamma % p.hkv;
     lam = gamma / p.hkv;
@@ -347,22 +347,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   const int ll = lam - E.group0 / p.hkv;
   const int s = ll % E.n_splits;
   const int mb = E.mb_hi - ll / E.n_splits;
-  const int h = g * G + hl;
 
   const int n_rows = E.n_rows;
   const int n_keys = E.n_keys;
-  const int row0 = mb * kAttnBM;
-  const int row_last = min(row0 + kAttnBM, n_rows) - 1;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  // this wave's query head and first row, and the workgroup's last row
+  int h, wrow0, row_last;
+  if (KIND == 1 && WPG == 1) {
+    // packed units (the split-key kernel always runs packed; with G = 1 the
+    // units of a workgroup are 4 consecutive row blocks of one head): unit u = (head hl_u, 32-row block rb_u), u = hl_u * n_rb + rb_u
+    const int n_rb = (n_rows + 31) / 32, n_units = G * n_rb;
+    const int u = mb * 4 + wave;
+    h = g * G + min(u, n_units - 1) / n_rb;
+    wrow0 = u < n_units ? (u % n_rb) * 32 : n_rows;  // a wave past the last unit has no rows
+    row_last = 0;
+    for (int j = 0; j < 4; ++j) {
+      const int uj = mb * 4 + j;
+      if (uj < n_units) row_last = max(row_last, min((uj % n_rb) * 32 + 31, n_rows - 1));
+    }
+  } else {
+    h = g * G + hl;
+    wrow0 = mb * kAttnBM + wave * 32;
+    row_last = min(mb * kAttnBM + kAttnBM, n_rows) - 1;
+  }
   const int k_begin = s * E.split_keys;
   const int k_end = min(min(k_begin + E.split_keys, n_keys), row_limit(E, row_last) + 1);
   const int n_tiles = k_end > k_begin ? (k_end - k_begin + kBN - 1) / kBN : 0;
 
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6;
   const int lane = tid & 63;
   const int l32 = lane & 31;
   const int half = lane >> 5;
-  const int wrow0 = row0 + wave * 32;
   const int my_row = wrow0 + l32;
   // keys above this are masked for the whole wave (a wave past the last row has none)
   const int wave_last_key = wrow0 < n_rows ? row_limit(E, wrow0 + 31) : -1;
@@ -433,7 +448,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   // barrier and no copy targets it any more.
   unsigned char *stg = ((n_tiles & 1) ? (wave < 2 ? k_lds1 : v_lds1) : (wave < 2 ? k_lds0 : v_lds0)) +
                        (wave & 1) * (TILE / 2);
-  const int wrow = row0 + wave * 32;  // first row of this wave
+  const int wrow = wrow0;  // first row of this wave
   if (E.n_splits == 1 && E.o != nullptr) {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -485,7 +500,7 @@ hipError_t launch_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
   } else {
     per_xcd = (p.n_groups + kXcds - 1) / kXcds;
   }
-  const int slots = p.group * per_xcd;
+  const int slots = p.wgs_per_group * per_xcd;
   const dim3 grid(kXcds * slots), block(kAttnThreads);
   switch (kind) {
     case AttnKind::kSelf: attn_bf16_kernel<D, 0><<<grid, block, 0, st>>>(p); break;

@@ -31,7 +31,7 @@ struct AttnEntry {
   int32_t lse_stride;
   int32_t n_rows;
   int32_t n_keys;
-  int32_t mb_hi;      // heaviest (last) query block of the range
+  int32_t mb_hi;      // heaviest (last) query block of the range (packed: unit group)
   int32_t mb_count;   // blocks mb_hi, mb_hi-1, ..., mb_hi-mb_count+1
   int32_t n_splits;   // key splits (1 = direct mode)
   int32_t split_keys; // keys per split, a multiple of the key tile
@@ -57,6 +57,11 @@ struct AttnLaunch;
 static_assert(sizeof(AttnEntry) * kMaxEntries + 64 < 4096, "attention launch table must fit 4 KiB of kernel arguments");
 struct AttnLaunch {
   int32_t hq, hkv, group;  // group = Hq / Hkv
+  // workgroups per work group: G (one query head each, 128 rows) or, for the
+  // bf16 split-key kernel, 1 (packed: the workgroup's 4 waves take 4
+  // consecutive (head, 32-row block) units of the KV group, so every K/V tile
+  // it copies serves several heads when the question is short)
+  int32_t wgs_per_group;
   int32_t n_entries;
   int32_t n_groups;        // total work groups over all entries
   float scale_log2;        // softmax scale * log2(e)
