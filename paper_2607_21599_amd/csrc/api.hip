@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "daf.h"
@@ -188,6 +189,36 @@ WsLayout ws_layout(const Cfg &c, const Batch &b, const std::vector<Split> &sp) {
   w.part_lse_bytes = align_up((size_t)w.part_rows * c.hq * sizeof(float));
   w.total = w.part_o_bytes + w.part_lse_bytes;
   return w;
+}
+
+// ---- second stream for the layer call ----------------------------------------
+// daf_layer_attn runs stage 1 on a library-owned stream (default priority),
+// forked from and joined back into the caller's stream by events, so that it
+// overlaps the KV write-back, stage 2 and the merge. One stream and two events
+// per device, created on first use; the mutex keeps each call's fork and join
+// together when several threads enqueue at once.
+struct AuxStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool tried = false, ok = false;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_aux_mu;
+AuxStream g_aux[kMaxDevices];
+
+// the current device's stream, or null (then the call runs on one stream);
+// call with g_aux_mu held
+AuxStream *aux_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  AuxStream &a = g_aux[dev];
+  if (!a.tried) {
+    a.tried = true;
+    a.ok = hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) == hipSuccess &&
+           hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess;
+  }
+  return a.ok ? &a : nullptr;
 }
 
 // ---- attention work tables ----------------------------------------------------
@@ -662,15 +693,33 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
     // the merge) to hidden[tok_b + L_d,b + j]
     add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, self, hidden, idx);
     CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, merge, o_q, lse_q, hidden));
-    // hybrid KV first (stage 2 reads it), then the attention stages and the
-    // split merge, whose epilogues also fuse the outputs into the hidden states
-    CHECK(fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr, nullptr,
-                    nullptr, stream));
-    // stage 2 then stage 1 as two grids: one grid holding both runs slower
-    // (stage 2's cache stream evicts the stage-1 K/V each XCD's L2 holds)
-    CHECK(run_entries(c, AttnKind::kQdoc, qdoc, stream));
-    CHECK(run_merge(c, merge, stream));
-    CHECK(run_entries(c, AttnKind::kSelf, self, stream));
+    // Stage 1 reads only the condensed q/k/v and writes o_imp and the
+    // important rows of hidden; the hybrid KV (which stage 2 reads), stage 2
+    // and the merge (question rows of hidden) touch none of that, so stage 1
+    // runs beside them on the second stream.
+    std::lock_guard<std::mutex> lock(g_aux_mu);
+    AuxStream *ax = self.empty() ? nullptr : aux_stream();
+    daf_status_t st1 = DAF_OK;
+    if (ax) {
+      hipError_t e = hipEventRecord(ax->fork, stream);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ax->s, ax->fork, 0);
+      if (e != hipSuccess) return hip_fail(e, "stream fork");
+      st1 = run_entries(c, AttnKind::kSelf, self, ax->s);
+    }
+    daf_status_t st = fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr,
+                                nullptr, nullptr, stream);
+    if (st == DAF_OK) st = run_entries(c, AttnKind::kQdoc, qdoc, stream);
+    if (st == DAF_OK) st = run_merge(c, merge, stream);
+    if (ax) {
+      // always join, so that nothing the caller's stream runs next can race stage 1
+      hipError_t e = hipEventRecord(ax->join, ax->s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(stream, ax->join, 0);
+      if (e != hipSuccess) return hip_fail(e, "stream join");
+    } else if (st == DAF_OK) {
+      st = run_entries(c, AttnKind::kSelf, self, stream);
+    }
+    CHECK(st1);
+    CHECK(st);
     return ok();
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");
