@@ -215,10 +215,13 @@ size_t daf_layer_workspace_size(const daf_attn_cfg_t *cfg,
 
 /* One DAF attention layer (Sec. 2 items 1-3), in the order the paper fixes:
  * hybrid KV write-back (DAF_FUSE_KV) first, then stage 2 (with its split
- * merge) and stage 1, all on `stream`. Arguments as in the stage calls. o_imp
- * and o_q receive the stage outputs; the same rows are written into `hidden`
- * exactly as DAF_FUSE_HIDDEN would (the state fusion happens in the stage
- * epilogues, without a separate pass). */
+ * merge); stage 1 needs none of these and runs beside them on a stream the
+ * library owns (one per device, default priority), forked from `stream` and
+ * joined back into it with events, so all of the call's work is ordered on
+ * `stream` for the caller. Arguments as in the stage calls. o_imp and o_q
+ * receive the stage outputs; the same rows are written into `hidden` exactly
+ * as DAF_FUSE_HIDDEN would (the state fusion happens in the stage epilogues,
+ * without a separate pass). */
 daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
                             const int32_t *idx, const void *q_imp,
                             const void *k_imp, const void *v_imp,
