@@ -284,3 +284,51 @@ def make_batch(shapes) -> Batch:
 
 def with_seed(s: Shape, seed: int, **kw) -> Shape:
     return replace(s, seed=seed, **kw)
+
+
+# ---- decoder-layer inputs (projections, norms, MLP around the attention) -------
+
+@dataclass
+class ModelShape:
+    """A decoder layer's widths (Qwen2.5-7B: hidden 3584, 28/4 heads of 128,
+    MLP 18944, RMSNorm eps 1e-6, RoPE base 1e6)."""
+    hidden: int = 3584
+    hq: int = 28
+    hkv: int = 4
+    d: int = 128
+    inter: int = 18944
+    eps: float = 1e-6
+    theta: float = 1e6
+
+
+QWEN7B = ModelShape()
+TINY_MODEL = ModelShape(hidden=256, hq=4, hkv=2, d=64, inter=512)
+
+
+def make_linear_case(M: int, N: int, K: int, seed: int, bias: bool = True, residual: bool = True):
+    """A [M][K] ~ N(0,1), W [N][K] ~ N(0, 1/K) (outputs of order 1), bias ~
+    N(0, 0.1^2), residual ~ N(0,1); all bf16 bit patterns."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    A = f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    W = f32_to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * np.float32(1.0 / np.sqrt(K)))
+    b = f32_to_bf16_bits(rng.standard_normal(N, dtype=np.float32) * np.float32(0.1)) if bias else None
+    R = f32_to_bf16_bits(rng.standard_normal((M, N), dtype=np.float32)) if residual else None
+    return A, W, b, R
+
+
+def make_layer_weights(m: ModelShape, seed: int) -> dict:
+    """Random weights of one decoder layer (bf16 bit patterns): projections
+    ~ N(0, 1/fan_in) so activations stay of order 1, biases ~ N(0, 0.1^2),
+    norm weights ~ 1 + N(0, 0.1^2). Projections are [out][in]."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+
+    def mat(o, i):
+        return f32_to_bf16_bits(rng.standard_normal((o, i), dtype=np.float32) * np.float32(1.0 / np.sqrt(i)))
+
+    def vec(n, mean, std):
+        return f32_to_bf16_bits(np.float32(mean) + rng.standard_normal(n, dtype=np.float32) * np.float32(std))
+
+    H, q, kv = m.hidden, m.hq * m.d, m.hkv * m.d
+    return dict(w_in=vec(H, 1.0, 0.1), wq=mat(q, H), bq=vec(q, 0.0, 0.1), wk=mat(kv, H), bk=vec(kv, 0.0, 0.1),
+                wv=mat(kv, H), bv=vec(kv, 0.0, 0.1), wo=mat(H, q), w_post=vec(H, 1.0, 0.1),
+                wg=mat(m.inter, H), wu=mat(m.inter, H), wd=mat(H, m.inter))
