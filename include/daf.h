@@ -240,6 +240,93 @@ daf_status_t daf_check_indices(const daf_batch_t *batch, const int32_t *idx,
 /* Static name of a status code. */
 const char *daf_status_string(daf_status_t status);
 
+/* Dense projection of the decoder layer around the attention: the QKV
+ * computation phase of Sec. 2 item 2 (run on the important and question rows
+ * only) and the projections that the fused compact state feeds (Sec. 2 item
+ * 3): C = A W^T (+ bias) (+ residual), bf16 in and out.
+ *   A [M][K] and W [N][K] row-major (W in the usual [out][in] layout);
+ *   bias [N] or NULL; residual [M][N] or NULL, and may be C itself (an
+ *   in-place residual add); C [M][N].
+ * fp32 accumulation; bias and residual are added in fp32 before the single
+ * rounding to bf16. N must be a positive multiple of 128 and K of 64
+ * (DAF_ERR_UNSUPPORTED otherwise); every pointer 16-byte aligned. M = 0 is a
+ * no-op. */
+daf_status_t daf_linear(int64_t M, int32_t N, int32_t K, const void *A,
+                        const void *W, const void *bias, const void *residual,
+                        void *C, hipStream_t stream);
+
+/* RMS normalisation before the projections: y = x / sqrt(mean(x^2) + eps) * w
+ * per row (x, y [rows][width], w [width], bf16; fp32 arithmetic). width must
+ * be a positive multiple of 8; y may be x. */
+daf_status_t daf_rmsnorm(int64_t rows, int32_t width, const void *x,
+                         const void *w, float eps, void *y, hipStream_t stream);
+
+/* Rotary position embedding, in place, of n_heads heads of head_dim features
+ * at the start of each of `rows` rows (row pitch row_stride elements, bf16):
+ * features (i, i + head_dim/2) of a head rotate by pos[row] *
+ * theta^(-2i/head_dim) (the angle in fp64). This is how the recomputed q and
+ * k of the important and question rows take their original positions
+ * (Sec. 2 item 1 keeps the original order). head_dim even, pos int32 [rows]. */
+daf_status_t daf_rope(int64_t rows, int32_t n_heads, int32_t head_dim,
+                      int64_t row_stride, void *x, const int32_t *pos,
+                      float theta, hipStream_t stream);
+
+/* MLP gate: out[r][j] = SiLU(gu[r][j]) * gu[r][width + j], SiLU(g) =
+ * g / (1 + exp(-g)); gu [rows][2 width] (gate then up), out [rows][width],
+ * bf16. width a positive multiple of 8. */
+daf_status_t daf_silu_mul(int64_t rows, int32_t width, const void *gu,
+                          void *out, hipStream_t stream);
+
+/* Weights of one decoder layer (bf16, projections [out][in]): the reading
+ * taken for the model the paper evaluates on (Qwen2.5-7B, Sec. 3) is the
+ * pre-norm decoder layer
+ *   h = RMSNorm(x) w_in; q,k,v = h W^T + b; RoPE(q, k); o = attention
+ *   x += o wo^T; h = RMSNorm(x) w_post; x += (SiLU(h wg^T) * (h wu^T)) wd^T */
+typedef struct {
+  const void *w_in;            /* [hidden] */
+  const void *wq, *bq;         /* [Hq*D][hidden], [Hq*D] */
+  const void *wk, *bk;         /* [Hkv*D][hidden], [Hkv*D] */
+  const void *wv, *bv;         /* [Hkv*D][hidden], [Hkv*D] */
+  const void *wo;              /* [hidden][Hq*D] */
+  const void *w_post;          /* [hidden] */
+  const void *wgu;             /* [2*inter][hidden]: the gate rows, then the up rows */
+  const void *wd;              /* [hidden][inter] */
+  int32_t hidden, inter;       /* multiples of 128 */
+  float eps, rope_theta;
+} daf_layer_weights_t;
+
+enum { DAF_LAYER_DAF = 0, DAF_LAYER_FULL = 1 };
+
+/* Workspace daf_decoder_layer needs (0 on bad input). */
+size_t daf_decoder_layer_workspace_size(const daf_attn_cfg_t *cfg,
+                                        const daf_layer_weights_t *w,
+                                        const daf_batch_t *batch,
+                                        int32_t mode);
+
+/* One decoder layer of prefill, in place on the residual stream x (bf16
+ * [rows][hidden]) at positions pos (int32 [rows]).
+ * DAF_LAYER_DAF (Sec. 2 items 1-3): only the important and question rows are
+ *   recomputed. rows = sum n + sum L_q, ordered as the stage calls take them:
+ *   every request's important rows (in idx order), then every request's
+ *   question rows. Their q/k/v come from the projections; the important and
+ *   question K/V are written into k_cache / v_cache (the hybrid cache, as
+ *   DAF_FUSE_KV) and the DAF attention runs as in daf_layer_attn; the other
+ *   document rows are not touched. The updated x is the compact state the
+ *   next layer takes (Sec. 2 item 3).
+ * DAF_LAYER_FULL (the full-recomputation baseline of Sec. 3): every token is
+ *   recomputed; rows = sum T_b, each request's documents then its question,
+ *   causal attention over the request's own rows; idx, k_cache and v_cache
+ *   are not used (may be NULL).
+ * workspace: at least daf_decoder_layer_workspace_size bytes, 256-byte
+ * aligned, contents undefined after the call. Errors as for the other calls;
+ * nothing is enqueued when a check fails. */
+daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg,
+                               const daf_layer_weights_t *w,
+                               const daf_batch_t *batch, int32_t mode,
+                               const int32_t *idx, const int32_t *pos, void *x,
+                               void *k_cache, void *v_cache, void *workspace,
+                               size_t ws_bytes, hipStream_t stream);
+
 /* Detail of the last failure on the calling thread ("" if none). */
 const char *daf_last_error(void);
 

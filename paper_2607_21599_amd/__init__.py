@@ -18,6 +18,8 @@ __all__ = [
     "DAF_FUSE_HIDDEN", "DafError", "AttnCfg", "Batch", "lib", "library_path",
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
+    "daf_linear", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
+    "daf_decoder_layer", "LayerWeights", "DAF_LAYER_DAF", "DAF_LAYER_FULL",
     "daf_status_string", "daf_last_error", "daf_version", "EXPORTED",
 ]
 
@@ -26,12 +28,14 @@ DAF_ERR_INVALID_ARG, DAF_ERR_ALIGNMENT, DAF_ERR_UNSUPPORTED, DAF_ERR_WORKSPACE, 
 DAF_BF16, DAF_F32 = 0, 1
 DAF_SRC_TOKENS, DAF_SRC_DOCS = 0, 1
 DAF_FUSE_KV, DAF_FUSE_HIDDEN = 1, 2
+DAF_LAYER_DAF, DAF_LAYER_FULL = 0, 1
 
 # every symbol include/daf.h declares
 EXPORTED = [
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
-    "daf_status_string", "daf_last_error", "daf_version",
+    "daf_linear", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
+    "daf_decoder_layer", "daf_status_string", "daf_last_error", "daf_version",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -75,8 +79,25 @@ class Batch:
         return cls([0, L_d], [0, L_q], [0, n])
 
 
-_lib = None
 _vp = ctypes.c_void_p
+
+
+class LayerWeights(ctypes.Structure):
+    """daf_layer_weights_t: device pointers of one decoder layer's weights.
+    Build it with ``from_tensors``, which keeps the tensors alive."""
+    _fields_ = [("w_in", _vp), ("wq", _vp), ("bq", _vp), ("wk", _vp), ("bk", _vp), ("wv", _vp), ("bv", _vp),
+                ("wo", _vp), ("w_post", _vp), ("wgu", _vp), ("wd", _vp), ("hidden", ctypes.c_int32),
+                ("inter", ctypes.c_int32), ("eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+
+    @classmethod
+    def from_tensors(cls, t: dict, hidden: int, inter: int, eps: float, rope_theta: float) -> "LayerWeights":
+        names = ["w_in", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "w_post", "wgu", "wd"]
+        w = cls(*[t[n].data_ptr() for n in names], hidden, inter, eps, rope_theta)
+        w._keep = t
+        return w
+
+
+_lib = None
 
 
 def lib() -> ctypes.CDLL:
@@ -101,6 +122,13 @@ def lib() -> ctypes.CDLL:
             "daf_layer_workspace_size": (sz, [cfgp, bp]),
             "daf_layer_attn": (i32, [cfgp, bp, _vp] + [_vp] * 13 + [_vp, sz, _vp]),
             "daf_check_indices": (i32, [bp, _vp, _vp, _vp]),
+            "daf_linear": (i32, [i64, i32, i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+            "daf_rmsnorm": (i32, [i64, i32, _vp, _vp, ctypes.c_float, _vp, _vp]),
+            "daf_rope": (i32, [i64, i32, i32, i64, _vp, _vp, ctypes.c_float, _vp]),
+            "daf_silu_mul": (i32, [i64, i32, _vp, _vp, _vp]),
+            "daf_decoder_layer_workspace_size": (sz, [cfgp, ctypes.POINTER(LayerWeights), bp, i32]),
+            "daf_decoder_layer": (i32, [cfgp, ctypes.POINTER(LayerWeights), bp, i32, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, sz, _vp]),
             "daf_status_string": (ctypes.c_char_p, [i32]),
             "daf_last_error": (ctypes.c_char_p, []),
             "daf_version": (i32, []),
@@ -165,6 +193,33 @@ def daf_imp_self_attn(cfg: AttnCfg, batch: Batch, q_imp, k_imp, v_imp, o_imp, ls
 def daf_position_attn(cfg: AttnCfg, n_rows: int, n_keys: int, q, q_pos, k, v, o, lse=None, stream=None):
     _check(lib().daf_position_attn(_cfgp(cfg), n_rows, n_keys, _ptr(q), _ptr(q_pos), _ptr(k), _ptr(v),
                                    _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def daf_linear(M: int, N: int, K: int, A, W, bias, residual, C, stream=None):
+    _check(lib().daf_linear(M, N, K, _ptr(A), _ptr(W), _ptr(bias), _ptr(residual), _ptr(C), _stream(stream)))
+
+
+def daf_rmsnorm(rows: int, width: int, x, w, eps: float, y, stream=None):
+    _check(lib().daf_rmsnorm(rows, width, _ptr(x), _ptr(w), eps, _ptr(y), _stream(stream)))
+
+
+def daf_rope(rows: int, n_heads: int, head_dim: int, row_stride: int, x, pos, theta: float, stream=None):
+    _check(lib().daf_rope(rows, n_heads, head_dim, row_stride, _ptr(x), _ptr(pos), theta, _stream(stream)))
+
+
+def daf_silu_mul(rows: int, width: int, gu, out, stream=None):
+    _check(lib().daf_silu_mul(rows, width, _ptr(gu), _ptr(out), _stream(stream)))
+
+
+def daf_decoder_layer_workspace_size(cfg: AttnCfg, w: LayerWeights, batch: Batch, mode: int) -> int:
+    return int(lib().daf_decoder_layer_workspace_size(_cfgp(cfg), ctypes.byref(w), ctypes.byref(batch.c), mode))
+
+
+def daf_decoder_layer(cfg: AttnCfg, w: LayerWeights, batch: Batch, mode: int, idx, pos, x, k_cache, v_cache,
+                      workspace, ws_bytes: int, stream=None):
+    _check(lib().daf_decoder_layer(_cfgp(cfg), ctypes.byref(w), ctypes.byref(batch.c), mode, _ptr(idx), _ptr(pos),
+                                   _ptr(x), _ptr(k_cache), _ptr(v_cache), _ptr(workspace), ws_bytes,
+                                   _stream(stream)))
 
 
 def daf_select_important(cfg: AttnCfg, batch: Batch, k_fresh, k_cached, scores, idx, stream=None):

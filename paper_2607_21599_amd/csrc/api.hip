@@ -444,6 +444,111 @@ daf_status_t check_fuse_ptrs(const Batch &b, uint32_t flags, const int32_t *idx,
   return DAF_OK;
 }
 
+// The layer's attention: hybrid KV write-back, stage 2 with its merge, and
+// stage 1 (on the second stream); with `hidden` set, the stage epilogues also
+// fuse the outputs into it. Pointers are checked by the caller.
+daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, const void *q_imp,
+                             const void *k_imp, const void *v_imp, const void *q_q, const void *k_q,
+                             const void *v_q, void *k_cache, void *v_cache, void *o_imp, float *lse_imp, void *o_q,
+                             float *lse_q, void *hidden, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  // plan (and check the workspace) before enqueueing anything
+  std::vector<AttnEntry> self, qdoc;
+  std::vector<MergeEntry> merge;
+  // the epilogues also fuse the outputs into the hidden states: stage-1 row i
+  // of request b goes to hidden[tok_b + idx[i]], question row j (written by
+  // the merge) to hidden[tok_b + L_d,b + j]
+  add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, self, hidden, idx);
+  CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, merge, o_q, lse_q, hidden));
+  // Stage 1 reads only the condensed q/k/v and writes o_imp and the
+  // important rows of hidden; the hybrid KV (which stage 2 reads), stage 2
+  // and the merge (question rows of hidden) touch none of that, so stage 1
+  // runs beside them on the second stream.
+  std::lock_guard<std::mutex> lock(g_aux_mu);
+  AuxStream *ax = self.empty() ? nullptr : aux_stream();
+  daf_status_t st1 = DAF_OK;
+  if (ax) {
+    hipError_t e = hipEventRecord(ax->fork, stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ax->s, ax->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "stream fork");
+    st1 = run_entries(c, AttnKind::kSelf, self, ax->s);
+  }
+  daf_status_t st = fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr,
+                              nullptr, nullptr, stream);
+  if (st == DAF_OK) st = run_entries(c, AttnKind::kQdoc, qdoc, stream);
+  if (st == DAF_OK) st = run_merge(c, merge, stream);
+  if (ax) {
+    // always join, so that nothing the caller's stream runs next can race stage 1
+    hipError_t e = hipEventRecord(ax->join, ax->s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(stream, ax->join, 0);
+    if (e != hipSuccess) return hip_fail(e, "stream join");
+  } else if (st == DAF_OK) {
+    st = run_entries(c, AttnKind::kSelf, self, stream);
+  }
+  CHECK(st1);
+  CHECK(st);
+  return ok();
+}
+
+// ---- decoder layer around the attention -------------------------------------
+struct LayerWs {
+  int64_t rows;
+  size_t h, q, k, v, o, gu, m, attn, attn_bytes, total;  // byte offsets, total size
+};
+
+daf_status_t check_weights(const Cfg &c, const daf_layer_weights_t *w) {
+  if (!w) return fail(DAF_ERR_INVALID_ARG, "weights is NULL");
+  if (c.dtype != DAF_BF16) return fail(DAF_ERR_UNSUPPORTED, "the decoder layer runs in bf16 only");
+  if (w->hidden <= 0 || w->hidden % 128 != 0 || w->inter <= 0 || w->inter % 128 != 0)
+    return fail(DAF_ERR_UNSUPPORTED, "hidden=%d and inter=%d must be positive multiples of 128", w->hidden,
+                w->inter);
+  if ((c.hq * c.d) % 128 != 0 || (c.hkv * c.d) % 128 != 0)
+    return fail(DAF_ERR_UNSUPPORTED, "Hq*D=%d and Hkv*D=%d must be multiples of 128", c.hq * c.d, c.hkv * c.d);
+  if (!(w->eps >= 0.f) || !(w->rope_theta > 0.f))
+    return fail(DAF_ERR_INVALID_ARG, "eps must be >= 0 and rope_theta > 0");
+  const void *p[] = {w->w_in, w->wq, w->bq, w->wk, w->bk, w->wv, w->bv, w->wo, w->w_post, w->wgu, w->wd};
+  const char *n[] = {"w_in", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "w_post", "wgu", "wd"};
+  for (int i = 0; i < 11; ++i) CHECK(need_ptr(p[i], n[i]));
+  return DAF_OK;
+}
+
+LayerWs layer_ws(const Cfg &c, const daf_layer_weights_t &w, const Batch &b, int mode) {
+  LayerWs l{};
+  l.rows = mode == DAF_LAYER_DAF ? b.total_imp + b.total_q : b.total_tok;
+  const size_t r = (size_t)l.rows, e = 2;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  l.h = take(r * w.hidden * e);
+  l.q = take(r * c.hq * c.d * e);
+  l.k = take(r * c.hkv * c.d * e);
+  l.v = take(r * c.hkv * c.d * e);
+  l.o = take(r * c.hq * c.d * e);
+  l.gu = take(r * 2 * w.inter * e);
+  l.m = take(r * w.inter * e);
+  l.attn_bytes = mode == DAF_LAYER_DAF ? ws_layout(c, b, plan_splits(c, b)).total : 0;
+  l.attn = take(l.attn_bytes);
+  l.total = off;
+  return l;
+}
+
+daf_status_t gemm(int64_t M, int N, int K, const void *A, const void *W, const void *bias, const void *res, void *C,
+                  hipStream_t st) {
+  GemmArgs g{};
+  g.A = A;
+  g.W = W;
+  g.bias = bias;
+  g.residual = res;
+  g.C = C;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  const hipError_t e = launch_gemm(g, st);
+  return e == hipSuccess ? DAF_OK : hip_fail(e, "linear launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -608,6 +713,186 @@ daf_status_t daf_select_important(const daf_attn_cfg_t *cfg, const daf_batch_t *
   }
 }
 
+daf_status_t daf_linear(int64_t M, int32_t N, int32_t K, const void *A, const void *W, const void *bias,
+                        const void *residual, void *C, hipStream_t stream) {
+  try {
+    if (M < 0) return fail(DAF_ERR_INVALID_ARG, "M=%lld is negative", (long long)M);
+    if (N <= 0 || N % 128 != 0) return fail(DAF_ERR_UNSUPPORTED, "N=%d is not a positive multiple of 128", N);
+    if (K <= 0 || K % 64 != 0) return fail(DAF_ERR_UNSUPPORTED, "K=%d is not a positive multiple of 64", K);
+    if ((int64_t)K * 2 * 128 > INT32_MAX) return fail(DAF_ERR_UNSUPPORTED, "K=%d too large", K);
+    if (M == 0) return ok();
+    CHECK(need_ptr(A, "A"));
+    CHECK(need_ptr(W, "W"));
+    CHECK(need_ptr(C, "C"));
+    if (bias) CHECK(need_ptr(bias, "bias"));
+    if (residual) CHECK(need_ptr(residual, "residual"));
+    GemmArgs g{};
+    g.A = A;
+    g.W = W;
+    g.bias = bias;
+    g.residual = residual;
+    g.C = C;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    const hipError_t e = launch_gemm(g, stream);
+    if (e != hipSuccess) return hip_fail(e, "linear launch");
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_rmsnorm(int64_t rows, int32_t width, const void *x, const void *w, float eps, void *y,
+                         hipStream_t stream) {
+  try {
+    if (rows < 0) return fail(DAF_ERR_INVALID_ARG, "rows=%lld is negative", (long long)rows);
+    if (width <= 0 || width % 8 != 0) return fail(DAF_ERR_UNSUPPORTED, "width=%d is not a positive multiple of 8", width);
+    if (!(eps >= 0.f)) return fail(DAF_ERR_INVALID_ARG, "eps must be >= 0");
+    if (rows == 0) return ok();
+    CHECK(need_ptr(x, "x"));
+    CHECK(need_ptr(w, "w"));
+    CHECK(need_ptr(y, "y"));
+    const hipError_t e = launch_rmsnorm(rows, width, x, w, eps, y, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "rmsnorm launch");
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_rope(int64_t rows, int32_t n_heads, int32_t head_dim, int64_t row_stride, void *x,
+                      const int32_t *pos, float theta, hipStream_t stream) {
+  try {
+    if (rows < 0) return fail(DAF_ERR_INVALID_ARG, "rows=%lld is negative", (long long)rows);
+    if (n_heads <= 0 || head_dim <= 0 || head_dim % 2 != 0)
+      return fail(DAF_ERR_INVALID_ARG, "n_heads=%d, head_dim=%d (head_dim must be even)", n_heads, head_dim);
+    if (row_stride < (int64_t)n_heads * head_dim)
+      return fail(DAF_ERR_INVALID_ARG, "row_stride=%lld is below n_heads * head_dim", (long long)row_stride);
+    if (!(theta > 0.f)) return fail(DAF_ERR_INVALID_ARG, "theta must be > 0");
+    if (rows == 0) return ok();
+    if (!x || !pos) return fail(DAF_ERR_INVALID_ARG, "x and pos must be non-NULL");
+    if (reinterpret_cast<uintptr_t>(x) % 2 != 0 || reinterpret_cast<uintptr_t>(pos) % 4 != 0)
+      return fail(DAF_ERR_ALIGNMENT, "x must be 2-byte and pos 4-byte aligned");
+    const hipError_t e = launch_rope(rows, n_heads, head_dim, row_stride, x, pos, theta, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "rope launch");
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+daf_status_t daf_silu_mul(int64_t rows, int32_t width, const void *gu, void *out, hipStream_t stream) {
+  try {
+    if (rows < 0) return fail(DAF_ERR_INVALID_ARG, "rows=%lld is negative", (long long)rows);
+    if (width <= 0 || width % 8 != 0) return fail(DAF_ERR_UNSUPPORTED, "width=%d is not a positive multiple of 8", width);
+    if (rows == 0) return ok();
+    CHECK(need_ptr(gu, "gu"));
+    CHECK(need_ptr(out, "out"));
+    const hipError_t e = launch_silu_mul(rows, width, gu, out, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "silu_mul launch");
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+size_t daf_decoder_layer_workspace_size(const daf_attn_cfg_t *cfg, const daf_layer_weights_t *w,
+                                        const daf_batch_t *batch, int32_t mode) {
+  try {
+    Cfg c;
+    Batch b;
+    if (parse_cfg(cfg, c) != DAF_OK || parse_batch(batch, b) != DAF_OK || !w) return 0;
+    if (mode != DAF_LAYER_DAF && mode != DAF_LAYER_FULL) return 0;
+    return layer_ws(c, *w, b, mode).total;
+  } catch (...) {
+    return 0;
+  }
+}
+
+daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weights_t *w, const daf_batch_t *batch,
+                               int32_t mode, const int32_t *idx, const int32_t *pos, void *x, void *k_cache,
+                               void *v_cache, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    CHECK(check_weights(c, w));
+    if (mode != DAF_LAYER_DAF && mode != DAF_LAYER_FULL)
+      return fail(DAF_ERR_INVALID_ARG, "mode=%d (use DAF_LAYER_DAF or DAF_LAYER_FULL)", mode);
+    CHECK(check_kv_extent(c, b));
+    const LayerWs l = layer_ws(c, *w, b, mode);
+    if (l.rows == 0) return ok();
+    CHECK(need_ptr(x, "x"));
+    if (!pos || reinterpret_cast<uintptr_t>(pos) % 4 != 0)
+      return fail(DAF_ERR_INVALID_ARG, "pos must be a non-NULL, 4-byte aligned int32 array");
+    if (mode == DAF_LAYER_DAF) {
+      if (b.total_imp > 0) CHECK(need_ptr(idx, "idx"));
+      CHECK(need_ptr(k_cache, "k_cache"));
+      CHECK(need_ptr(v_cache, "v_cache"));
+    }
+    if (!workspace) return fail(DAF_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", l.total);
+    if (ws_bytes < l.total) return fail(DAF_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, l.total);
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+      return fail(DAF_ERR_ALIGNMENT, "workspace is not %zu-byte aligned", kAlign);
+    char *ws = static_cast<char *>(workspace);
+    void *h = ws + l.h, *q = ws + l.q, *k = ws + l.k, *v = ws + l.v, *o = ws + l.o, *gu = ws + l.gu, *m = ws + l.m;
+    const int64_t R = l.rows;
+    const int H = w->hidden, I = w->inter, QW = c.hq * c.d, KW = c.hkv * c.d;
+    const hipError_t e0 = launch_rmsnorm(R, H, x, w->w_in, w->eps, h, stream);
+    if (e0 != hipSuccess) return hip_fail(e0, "rmsnorm launch");
+    CHECK(gemm(R, QW, H, h, w->wq, w->bq, nullptr, q, stream));
+    CHECK(gemm(R, KW, H, h, w->wk, w->bk, nullptr, k, stream));
+    CHECK(gemm(R, KW, H, h, w->wv, w->bv, nullptr, v, stream));
+    hipError_t e1 = launch_rope(R, c.hq, c.d, QW, q, pos, w->rope_theta, stream);
+    if (e1 == hipSuccess) e1 = launch_rope(R, c.hkv, c.d, KW, k, pos, w->rope_theta, stream);
+    if (e1 != hipSuccess) return hip_fail(e1, "rope launch");
+    if (mode == DAF_LAYER_DAF) {
+      const int64_t ni = b.total_imp;
+      char *qb = static_cast<char *>(q), *kb = static_cast<char *>(k), *vb = static_cast<char *>(v);
+      char *ob = static_cast<char *>(o);
+      CHECK(layer_attn_impl(c, b, idx, qb, kb, vb, qb + ni * QW * 2, kb + ni * KW * 2, vb + ni * KW * 2, k_cache,
+                            v_cache, ob, nullptr, ob + ni * QW * 2, nullptr, nullptr, ws + l.attn, l.attn_bytes,
+                            stream));
+    } else {
+      // every token recomputed: causal attention over each request's own rows
+      std::vector<int> order;
+      for (int i = 0; i < (int)b.r.size(); ++i)
+        if (b.r[i].L_d + b.r[i].L_q > 0) order.push_back(i);
+      std::stable_sort(order.begin(), order.end(), [&](int a, int bb) {
+        return b.r[a].L_d + b.r[a].L_q > b.r[bb].L_d + b.r[bb].L_q;
+      });
+      std::vector<AttnEntry> entries;
+      for (int i : order) {
+        const Req &r = b.r[i];
+        const int T = r.L_d + r.L_q;
+        AttnEntry e{};
+        e.q = static_cast<char *>(q) + r.tok0 * QW * 2;
+        e.k = static_cast<char *>(k) + r.tok0 * KW * 2;
+        e.v = static_cast<char *>(v) + r.tok0 * KW * 2;
+        e.o = static_cast<char *>(o) + r.tok0 * QW * 2;
+        e.n_rows = T;
+        e.n_keys = T;
+        const int mbs = (T + kAttnBM - 1) / kAttnBM;
+        e.mb_hi = mbs - 1;
+        e.mb_count = mbs;
+        e.n_splits = 1;
+        e.split_keys = (T + c.key_tile - 1) / c.key_tile * c.key_tile;
+        entries.push_back(e);
+      }
+      CHECK(run_entries(c, AttnKind::kSelf, entries, stream));
+    }
+    CHECK(gemm(R, H, QW, o, w->wo, nullptr, x, x, stream));
+    const hipError_t e2 = launch_rmsnorm(R, H, x, w->w_post, w->eps, h, stream);
+    if (e2 != hipSuccess) return hip_fail(e2, "rmsnorm launch");
+    CHECK(gemm(R, 2 * I, H, h, w->wgu, nullptr, nullptr, gu, stream));
+    const hipError_t e3 = launch_silu_mul(R, I, gu, m, stream);
+    if (e3 != hipSuccess) return hip_fail(e3, "silu_mul launch");
+    CHECK(gemm(R, H, I, m, w->wd, nullptr, x, x, stream));
+    return ok();
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
 size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg, const daf_batch_t *batch) {
   try {
     Cfg c;
@@ -685,42 +970,8 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
     if (b.total_q > 0) CHECK(need_ptr(q_q, "q_q"));
     if (lse_imp) CHECK(need_ptr(lse_imp, "lse_imp"));
     if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
-    // plan (and check the workspace) before enqueueing anything
-    std::vector<AttnEntry> self, qdoc;
-    std::vector<MergeEntry> merge;
-    // the epilogues also fuse the outputs into the hidden states: stage-1 row i
-    // of request b goes to hidden[tok_b + idx[i]], question row j (written by
-    // the merge) to hidden[tok_b + L_d,b + j]
-    add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, self, hidden, idx);
-    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, merge, o_q, lse_q, hidden));
-    // Stage 1 reads only the condensed q/k/v and writes o_imp and the
-    // important rows of hidden; the hybrid KV (which stage 2 reads), stage 2
-    // and the merge (question rows of hidden) touch none of that, so stage 1
-    // runs beside them on the second stream.
-    std::lock_guard<std::mutex> lock(g_aux_mu);
-    AuxStream *ax = self.empty() ? nullptr : aux_stream();
-    daf_status_t st1 = DAF_OK;
-    if (ax) {
-      hipError_t e = hipEventRecord(ax->fork, stream);
-      if (e == hipSuccess) e = hipStreamWaitEvent(ax->s, ax->fork, 0);
-      if (e != hipSuccess) return hip_fail(e, "stream fork");
-      st1 = run_entries(c, AttnKind::kSelf, self, ax->s);
-    }
-    daf_status_t st = fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr,
-                                nullptr, nullptr, stream);
-    if (st == DAF_OK) st = run_entries(c, AttnKind::kQdoc, qdoc, stream);
-    if (st == DAF_OK) st = run_merge(c, merge, stream);
-    if (ax) {
-      // always join, so that nothing the caller's stream runs next can race stage 1
-      hipError_t e = hipEventRecord(ax->join, ax->s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(stream, ax->join, 0);
-      if (e != hipSuccess) return hip_fail(e, "stream join");
-    } else if (st == DAF_OK) {
-      st = run_entries(c, AttnKind::kSelf, self, stream);
-    }
-    CHECK(st1);
-    CHECK(st);
-    return ok();
+    return layer_attn_impl(c, b, idx, q_imp, k_imp, v_imp, q_q, k_q, v_q, k_cache, v_cache, o_imp, lse_imp, o_q,
+                           lse_q, hidden, workspace, ws_bytes, stream);
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");
   }

@@ -155,4 +155,22 @@ hipError_t launch_check_indices(const RowLaunch &p, int32_t *d_bad,
 hipError_t launch_select_scores(const SelectLaunch &p, bool bf16, hipStream_t st);
 hipError_t launch_select_topn(const SelectLaunch &p, hipStream_t st);
 
+// ---- dense projections (C = A W^T + bias + residual, bf16) -------------------
+struct GemmArgs {
+  const void *A;         // [M][K]
+  const void *W;         // [N][K]
+  const void *bias;      // [N] or null
+  const void *residual;  // [M][N] or null (may be C itself)
+  void *C;               // [M][N]
+  int64_t M;
+  int32_t N, K;          // N % 128 == 0, K % 64 == 0
+  int32_t tiles_m, tiles_n;  // filled by launch_gemm
+};
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t st);
+hipError_t launch_rmsnorm(int64_t rows, int width, const void *x, const void *w, float eps, void *y,
+                          hipStream_t st);
+hipError_t launch_rope(int64_t rows, int heads, int d, int64_t row_stride, void *x, const int32_t *pos,
+                       double theta, hipStream_t st);
+hipError_t launch_silu_mul(int64_t rows, int width, const void *gu, void *out, hipStream_t st);
+
 }  // namespace daf

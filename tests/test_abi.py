@@ -163,3 +163,58 @@ def test_select_important_checks():
                                  FAKE, FAKE, 0)
     assert e.value.status == daf.DAF_ERR_UNSUPPORTED
     daf.daf_select_important(c, daf.Batch.single(0, 3, 0), [FAKE], [FAKE], None, None, 0)  # no documents
+
+
+def _weights(**kw):
+    a = dict(hidden=256, inter=512, eps=1e-6, rope_theta=1e6)
+    a.update(kw)
+    return daf.LayerWeights(*([FAKE] * 11), a["hidden"], a["inter"], a["eps"], a["rope_theta"])
+
+
+def _status(fn, *args):
+    with pytest.raises(daf.DafError) as e:
+        fn(*args)
+    return e.value.status
+
+
+def test_linear_and_row_op_checks():
+    assert _status(daf.daf_linear, 10, 100, 64, FAKE, FAKE, None, None, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+    assert _status(daf.daf_linear, 10, 128, 96, FAKE, FAKE, None, None, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+    assert _status(daf.daf_linear, -1, 128, 64, FAKE, FAKE, None, None, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
+    assert _status(daf.daf_linear, 10, 128, 64, None, FAKE, None, None, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
+    assert _status(daf.daf_linear, 10, 128, 64, FAKE, FAKE, FAKE + 2, None, FAKE, 0) == daf.DAF_ERR_ALIGNMENT
+    daf.daf_linear(0, 128, 64, None, None, None, None, None, 0)  # no rows: nothing to do
+    assert _status(daf.daf_rmsnorm, 4, 12, FAKE, FAKE, 1e-6, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+    assert _status(daf.daf_rmsnorm, 4, 16, FAKE, FAKE, -1.0, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
+    daf.daf_rmsnorm(0, 16, None, None, 1e-6, None, 0)
+    assert _status(daf.daf_rope, 4, 2, 63, 128, FAKE, FAKE, 1e4, 0) == daf.DAF_ERR_INVALID_ARG
+    assert _status(daf.daf_rope, 4, 2, 64, 100, FAKE, FAKE, 1e4, 0) == daf.DAF_ERR_INVALID_ARG
+    assert _status(daf.daf_rope, 4, 2, 64, 128, FAKE, FAKE, 0.0, 0) == daf.DAF_ERR_INVALID_ARG
+    assert _status(daf.daf_rope, 4, 2, 64, 128, FAKE, FAKE + 2, 1e4, 0) == daf.DAF_ERR_ALIGNMENT
+    assert _status(daf.daf_silu_mul, 4, 12, FAKE, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+
+
+def test_decoder_layer_checks():
+    c = _cfg(n_q_heads=4, n_kv_heads=2, head_dim=64)
+    b = daf.Batch.single(600, 32, 90)
+    w = _weights()
+    L = daf.daf_decoder_layer
+    ws = daf.daf_decoder_layer_workspace_size(c, w, b, daf.DAF_LAYER_DAF)
+    assert ws > 0 and daf.daf_decoder_layer_workspace_size(c, w, b, 7) == 0
+    full = daf.daf_decoder_layer_workspace_size(c, w, b, daf.DAF_LAYER_FULL)
+    assert full > ws  # every token recomputed
+    args = (daf.DAF_LAYER_DAF, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 0)
+    assert _status(L, _cfg(n_q_heads=4, n_kv_heads=2, head_dim=64, dtype=daf.DAF_F32), w, b, *args) == \
+        daf.DAF_ERR_UNSUPPORTED
+    assert _status(L, c, _weights(hidden=200), b, *args) == daf.DAF_ERR_UNSUPPORTED
+    bad = _weights()
+    bad.wo = None
+    assert _status(L, c, bad, b, *args) == daf.DAF_ERR_INVALID_ARG
+    assert _status(L, c, w, b, 5, *args[1:]) == daf.DAF_ERR_INVALID_ARG
+    assert _status(L, c, w, b, *args[:-2], ws - 1, 0) == daf.DAF_ERR_WORKSPACE
+    assert _status(L, c, w, b, daf.DAF_LAYER_DAF, FAKE, None, FAKE, FAKE, FAKE, FAKE, ws, 0) == \
+        daf.DAF_ERR_INVALID_ARG  # no positions
+    # the full layer needs no cache or indices
+    assert _status(L, c, w, b, daf.DAF_LAYER_FULL, None, FAKE, FAKE, None, None, FAKE, full - 1, 0) == \
+        daf.DAF_ERR_WORKSPACE
+    L(c, w, daf.Batch.single(0, 0, 0), daf.DAF_LAYER_DAF, None, None, None, None, None, None, 0, 0)  # no rows
