@@ -142,6 +142,83 @@ def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
                         "attention times scaled by total/sampled rows"))
 
 
+def decoder_layer_section(s0, batch, spin_cycles: int, selection_us) -> dict:
+    """One prefill decoder layer with Qwen2.5-7B-shaped synthetic weights:
+    DAF (only the important and question rows, DAF attention on the hybrid
+    cache) against full recomputation (every row, causal attention), each
+    call timed alone behind a GPU spin, and a 28-layer TTFT model from them."""
+    import torch
+
+    import paper_2607_21599_amd as daf
+    m = di.QWEN7B
+    H, I, QW, KW = m.hidden, m.inter, m.hq * m.d, m.hkv * m.d
+    g = torch.Generator(device="cuda")
+    g.manual_seed(20240607)
+
+    def randn(*shape, std=1.0, mean=0.0):
+        return (torch.randn(*shape, generator=g, device="cuda") * std + mean).to(torch.bfloat16)
+
+    wt = dict(w_in=randn(H, std=0.1, mean=1.0), wq=randn(QW, H, std=H ** -0.5), bq=randn(QW, std=0.1),
+              wk=randn(KW, H, std=H ** -0.5), bk=randn(KW, std=0.1), wv=randn(KW, H, std=H ** -0.5),
+              bv=randn(KW, std=0.1), wo=randn(H, QW, std=QW ** -0.5), w_post=randn(H, std=0.1, mean=1.0),
+              wgu=randn(2 * I, H, std=H ** -0.5), wd=randn(H, I, std=I ** -0.5))
+    lw = daf.LayerWeights.from_tensors(wt, H, I, m.eps, m.theta)
+    cfg = daf.AttnCfg(m.hq, m.hkv, m.d, daf.DAF_BF16)
+    L_d, L_q, n, T = s0.L_d, s0.L_q, s0.n, s0.T
+    idx = batch.request(0)["idx"].astype(np.int32)
+    rows_act = np.concatenate([idx, np.arange(L_d, T, dtype=np.int32)])
+    x_all = randn(T, H)
+    modes = {
+        "daf": dict(mode=daf.DAF_LAYER_DAF, b=daf.Batch.single(L_d, L_q, n), x0=x_all[torch.from_numpy(rows_act).
+                    long().cuda()].contiguous(), pos=torch.from_numpy(rows_act).cuda(),
+                    idx=torch.from_numpy(idx).cuda(), kc=randn(T, m.hkv, m.d, std=0.5),
+                    vc=randn(T, m.hkv, m.d, std=0.5), reps=5),
+        "full": dict(mode=daf.DAF_LAYER_FULL, b=daf.Batch.single(L_d, L_q, 0), x0=x_all,
+                     pos=torch.arange(T, dtype=torch.int32, device="cuda"), idx=None, kc=None, vc=None, reps=3),
+    }
+    res = {}
+    for name, c in modes.items():
+        ws_bytes = daf.daf_decoder_layer_workspace_size(cfg, lw, c["b"], c["mode"])
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        x = c["x0"].clone()
+
+        def run():
+            daf.daf_decoder_layer(cfg, lw, c["b"], c["mode"], c["idx"], c["pos"], x, c["kc"], c["vc"], ws,
+                                  ws_bytes)
+        run()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(c["reps"]):
+            x.copy_(c["x0"])
+            torch.cuda._sleep(spin_cycles)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            run()
+            b.record()
+            torch.cuda.synchronize()
+            t.append(a.elapsed_time(b) * 1e3)
+        rows = c["x0"].shape[0]
+        gemm_flop = 2 * rows * H * (QW + 2 * KW + QW + 2 * I + I)
+        res[name] = dict(us=float(np.mean(t)), rows=int(rows), gemm_flop=int(gemm_flop))
+        del ws
+    n_full_layers, n_layers = 4, 28  # layers 1-4 recomputed in full for the selection signal (layers 2-4)
+    sel = selection_us or 0.0
+    ttft_daf = n_full_layers * res["full"]["us"] + sel + (n_layers - n_full_layers) * res["daf"]["us"]
+    ttft_full = n_layers * res["full"]["us"]
+    return {
+        "model": "Qwen2.5-7B-shaped layer, synthetic bf16 weights (hidden 3584, 28/4 heads, MLP 18944)",
+        "daf_layer_us": res["daf"]["us"], "daf_rows": res["daf"]["rows"],
+        "full_layer_us": res["full"]["us"], "full_rows": res["full"]["rows"],
+        "layer_speedup": res["full"]["us"] / res["daf"]["us"],
+        "daf_gemm_flop": res["daf"]["gemm_flop"], "full_gemm_flop": res["full"]["gemm_flop"],
+        "ttft_model_ms": {"daf": ttft_daf / 1e3, "full_recompute": ttft_full / 1e3,
+                          "speedup": ttft_full / ttft_daf,
+                          "recipe": f"{n_full_layers} full layers (selection signal) + selection + "
+                                    f"{n_layers - n_full_layers} DAF layers, vs {n_layers} full layers; "
+                                    "no embedding, LM head or KV loading"},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +229,8 @@ def main():
     ap.add_argument("--cpu-stride1", type=int, default=4)
     ap.add_argument("--cpu-stride2", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-layer", action="store_true",
+                    help="skip the decoder-layer section (projections, norms and MLP around the attention)")
     ap.add_argument("--no-patterns", action="store_true",
                     help="skip the comparison patterns (CacheBlend-style and full recomputation attention)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -353,6 +432,11 @@ def main():
                     "the paper's Table 1 speedups are end-to-end TTFT on an A100",
         }
 
+    layer = None
+    if not args.no_layer and len(shapes) == 1 and s0.dtype == di.BF16:
+        print("[bench] decoder layer: DAF vs full recomputation", file=sys.stderr, flush=True)
+        layer = decoder_layer_section(s0, batch, spin_cycles, selection["us"] if selection else None)
+
     out = {
         "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
@@ -370,6 +454,8 @@ def main():
         out["selection"] = selection
     if comparison is not None:
         out["comparison"] = comparison
+    if layer is not None:
+        out["decoder_layer"] = layer
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(batch, args.cpu_stride1, args.cpu_stride2)
