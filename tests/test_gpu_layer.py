@@ -60,20 +60,22 @@ def test_linear(M, N, K, bias, res):
     assert torch.all(C[M:] == 7.0), "rows past M were written"
 
 
-@pytest.mark.parametrize("N,K", [(4608, 3584), (3584, 18944)])
-def test_linear_full_size_sampled(N, K):
-    """The layer's QKV and down projections at the 32k shape (n + L_q = 5043
-    rows), oracle on sampled rows."""
+@pytest.mark.parametrize("M,N,K,res", [(5043, 4608, 3584, False), (5043, 3584, 18944, False),
+                                       (5043, 37888, 3584, False), (2100, 14848, 512, True)])
+def test_linear_full_size_sampled(M, N, K, res):
+    """The layer's QKV, down and gate+up projections at the 32k shape
+    (n + L_q = 5043 rows; gate+up and the last case take the 256 x 256 tile,
+    the last one with a ragged M and an in-place residual), oracle on sampled
+    rows."""
     import paper_2607_21599_amd as daf
-    M = 5043
-    A, W, b, _ = di.make_linear_case(M, N, K, seed=N + K, bias=True, residual=False)
-    C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    daf.daf_linear(M, N, K, _dev(A), _dev(W), _dev(b), None, C)
+    A, W, b, R = di.make_linear_case(M, N, K, seed=N + K, bias=True, residual=res)
+    C = _dev(R) if res else torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    daf.daf_linear(M, N, K, _dev(A), _dev(W), _dev(b), C if res else None, C)
     torch.cuda.synchronize()
     rows = np.sort(np.random.Generator(np.random.PCG64(1)).choice(M, 24, replace=False))
-    rows = np.union1d(rows, [0, M - 1])
+    rows = np.union1d(rows, [0, 255, 256, M - 1])
     w = di.raw_to_f32
-    ref = dec.linear(w(A[rows]), w(W), w(b))
+    ref = dec.linear(w(A[rows]), w(W), w(b), w(R[rows]) if res else None)
     _close(_f(C[torch.from_numpy(rows).cuda()]), ref, f"linear {M}x{N}x{K}")
 
 
