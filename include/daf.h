@@ -255,6 +255,14 @@ daf_status_t daf_linear(int64_t M, int32_t N, int32_t K, const void *A,
                         const void *W, const void *bias, const void *residual,
                         void *C, hipStream_t stream);
 
+/* The MLP's gate and up projections with the gate applied in the epilogue:
+ * C[m][j] = SiLU((A Wg^T)[m][j]) * (A Wu^T)[m][j], SiLU(g) = g / (1 + exp(-g)),
+ * where Wgu [2I][K] holds the gate rows then the up rows (bf16, fp32
+ * accumulation, one rounding). A [M][K], C [M][I]. I a positive multiple of
+ * 64 and K of 64 (DAF_ERR_UNSUPPORTED otherwise); pointers 16-byte aligned. */
+daf_status_t daf_linear_swiglu(int64_t M, int32_t I, int32_t K, const void *A,
+                               const void *Wgu, void *C, hipStream_t stream);
+
 /* RMS normalisation before the projections: y = x / sqrt(mean(x^2) + eps) * w
  * per row (x, y [rows][width], w [width], bf16; fp32 arithmetic). width must
  * be a positive multiple of 8; y may be x. */

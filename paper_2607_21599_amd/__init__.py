@@ -18,7 +18,7 @@ __all__ = [
     "DAF_FUSE_HIDDEN", "DafError", "AttnCfg", "Batch", "lib", "library_path",
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
-    "daf_linear", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
+    "daf_linear", "daf_linear_swiglu", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
     "daf_decoder_layer", "LayerWeights", "DAF_LAYER_DAF", "DAF_LAYER_FULL",
     "daf_status_string", "daf_last_error", "daf_version", "EXPORTED",
 ]
@@ -34,7 +34,7 @@ DAF_LAYER_DAF, DAF_LAYER_FULL = 0, 1
 EXPORTED = [
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
     "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
-    "daf_linear", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
+    "daf_linear", "daf_linear_swiglu", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
     "daf_decoder_layer", "daf_status_string", "daf_last_error", "daf_version",
 ]
 
@@ -123,6 +123,7 @@ def lib() -> ctypes.CDLL:
             "daf_layer_attn": (i32, [cfgp, bp, _vp] + [_vp] * 13 + [_vp, sz, _vp]),
             "daf_check_indices": (i32, [bp, _vp, _vp, _vp]),
             "daf_linear": (i32, [i64, i32, i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+            "daf_linear_swiglu": (i32, [i64, i32, i32, _vp, _vp, _vp, _vp]),
             "daf_rmsnorm": (i32, [i64, i32, _vp, _vp, ctypes.c_float, _vp, _vp]),
             "daf_rope": (i32, [i64, i32, i32, i64, _vp, _vp, ctypes.c_float, _vp]),
             "daf_silu_mul": (i32, [i64, i32, _vp, _vp, _vp]),
@@ -197,6 +198,10 @@ def daf_position_attn(cfg: AttnCfg, n_rows: int, n_keys: int, q, q_pos, k, v, o,
 
 def daf_linear(M: int, N: int, K: int, A, W, bias, residual, C, stream=None):
     _check(lib().daf_linear(M, N, K, _ptr(A), _ptr(W), _ptr(bias), _ptr(residual), _ptr(C), _stream(stream)))
+
+
+def daf_linear_swiglu(M: int, I: int, K: int, A, Wgu, C, stream=None):
+    _check(lib().daf_linear_swiglu(M, I, K, _ptr(A), _ptr(Wgu), _ptr(C), _stream(stream)))
 
 
 def daf_rmsnorm(rows: int, width: int, x, w, eps: float, y, stream=None):

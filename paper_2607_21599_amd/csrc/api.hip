@@ -493,7 +493,7 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
 // ---- decoder layer around the attention -------------------------------------
 struct LayerWs {
   int64_t rows;
-  size_t h, q, k, v, o, gu, m, attn, attn_bytes, total;  // byte offsets, total size
+  size_t h, q, k, v, o, m, attn, attn_bytes, total;  // byte offsets, total size
 };
 
 daf_status_t check_weights(const Cfg &c, const daf_layer_weights_t *w) {
@@ -502,6 +502,8 @@ daf_status_t check_weights(const Cfg &c, const daf_layer_weights_t *w) {
   if (w->hidden <= 0 || w->hidden % 128 != 0 || w->inter <= 0 || w->inter % 128 != 0)
     return fail(DAF_ERR_UNSUPPORTED, "hidden=%d and inter=%d must be positive multiples of 128", w->hidden,
                 w->inter);
+  if (((int64_t)w->inter + 256) * w->hidden * 2 > INT32_MAX || (int64_t)w->hidden * w->inter * 2 > INT32_MAX)
+    return fail(DAF_ERR_UNSUPPORTED, "hidden=%d x inter=%d too large", w->hidden, w->inter);
   if ((c.hq * c.d) % 128 != 0 || (c.hkv * c.d) % 128 != 0)
     return fail(DAF_ERR_UNSUPPORTED, "Hq*D=%d and Hkv*D=%d must be multiples of 128", c.hq * c.d, c.hkv * c.d);
   if (!(w->eps >= 0.f) || !(w->rope_theta > 0.f))
@@ -527,7 +529,6 @@ LayerWs layer_ws(const Cfg &c, const daf_layer_weights_t &w, const Batch &b, int
   l.k = take(r * c.hkv * c.d * e);
   l.v = take(r * c.hkv * c.d * e);
   l.o = take(r * c.hq * c.d * e);
-  l.gu = take(r * 2 * w.inter * e);
   l.m = take(r * w.inter * e);
   l.attn_bytes = mode == DAF_LAYER_DAF ? ws_layout(c, b, plan_splits(c, b)).total : 0;
   l.attn = take(l.attn_bytes);
@@ -744,6 +745,32 @@ daf_status_t daf_linear(int64_t M, int32_t N, int32_t K, const void *A, const vo
   }
 }
 
+daf_status_t daf_linear_swiglu(int64_t M, int32_t I, int32_t K, const void *A, const void *Wgu, void *C,
+                               hipStream_t stream) {
+  try {
+    if (M < 0) return fail(DAF_ERR_INVALID_ARG, "M=%lld is negative", (long long)M);
+    if (I <= 0 || I % 64 != 0) return fail(DAF_ERR_UNSUPPORTED, "I=%d is not a positive multiple of 64", I);
+    if (K <= 0 || K % 64 != 0) return fail(DAF_ERR_UNSUPPORTED, "K=%d is not a positive multiple of 64", K);
+    if (((int64_t)I + 256) * K * 2 > INT32_MAX) return fail(DAF_ERR_UNSUPPORTED, "I*K too large");
+    if (M == 0) return ok();
+    CHECK(need_ptr(A, "A"));
+    CHECK(need_ptr(Wgu, "Wgu"));
+    CHECK(need_ptr(C, "C"));
+    GemmArgs g{};
+    g.A = A;
+    g.W = Wgu;
+    g.C = C;
+    g.M = M;
+    g.N = I;
+    g.K = K;
+    g.glu = 1;
+    const hipError_t e = launch_gemm(g, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "linear launch");
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
 daf_status_t daf_rmsnorm(int64_t rows, int32_t width, const void *x, const void *w, float eps, void *y,
                          hipStream_t stream) {
   try {
@@ -835,7 +862,7 @@ daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weight
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
       return fail(DAF_ERR_ALIGNMENT, "workspace is not %zu-byte aligned", kAlign);
     char *ws = static_cast<char *>(workspace);
-    void *h = ws + l.h, *q = ws + l.q, *k = ws + l.k, *v = ws + l.v, *o = ws + l.o, *gu = ws + l.gu, *m = ws + l.m;
+    void *h = ws + l.h, *q = ws + l.q, *k = ws + l.k, *v = ws + l.v, *o = ws + l.o, *m = ws + l.m;
     const int64_t R = l.rows;
     const int H = w->hidden, I = w->inter, QW = c.hq * c.d, KW = c.hkv * c.d;
     const hipError_t e0 = launch_rmsnorm(R, H, x, w->w_in, w->eps, h, stream);
@@ -884,9 +911,18 @@ daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weight
     CHECK(gemm(R, H, QW, o, w->wo, nullptr, x, x, stream));
     const hipError_t e2 = launch_rmsnorm(R, H, x, w->w_post, w->eps, h, stream);
     if (e2 != hipSuccess) return hip_fail(e2, "rmsnorm launch");
-    CHECK(gemm(R, 2 * I, H, h, w->wgu, nullptr, nullptr, gu, stream));
-    const hipError_t e3 = launch_silu_mul(R, I, gu, m, stream);
-    if (e3 != hipSuccess) return hip_fail(e3, "silu_mul launch");
+    {  // gate and up projections with SiLU(gate) * up in the epilogue
+      GemmArgs g{};
+      g.A = h;
+      g.W = w->wgu;
+      g.C = m;
+      g.M = R;
+      g.N = I;
+      g.K = H;
+      g.glu = 1;
+      const hipError_t e3 = launch_gemm(g, stream);
+      if (e3 != hipSuccess) return hip_fail(e3, "linear launch");
+    }
     CHECK(gemm(R, H, I, m, w->wd, nullptr, x, x, stream));
     return ok();
   } catch (...) {

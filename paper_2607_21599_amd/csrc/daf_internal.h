@@ -163,7 +163,10 @@ struct GemmArgs {
   const void *residual;  // [M][N] or null (may be C itself)
   void *C;               // [M][N]
   int64_t M;
-  int32_t N, K;          // N % 128 == 0, K % 64 == 0
+  int32_t N, K;          // N % 128 == 0 (glu: N % 64 == 0), K % 64 == 0
+  // glu: W is [2N][K], the gate rows then the up rows, and C[m][j] =
+  // SiLU((A W^T)[m][j]) * (A W^T)[m][N + j] (no bias or residual)
+  int32_t glu;
   int32_t tiles_m, tiles_n;  // filled by launch_gemm
 };
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t st);

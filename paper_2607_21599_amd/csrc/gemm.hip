@@ -100,7 +100,7 @@ __device__ __forceinline__ void mma_step(f32x16 (&acc)[S::MB][S::NB], const unsi
 }
 
 template <class S>
-__device__ __forceinline__ void k_step(f32x16 (&acc)[S::MB][S::NB], const GemmArgs &p, const unsigned char *as,
+__device__ __forceinline__ void k_step(f32x16 (&acc)[S::MB][S::NB], int b_rows_bytes, const unsigned char *as,
                                        const unsigned char *bs, unsigned char *an, unsigned char *bn,
                                        const unsigned char *Ab, const unsigned char *Wb, int a_rows_bytes, int kt,
                                        bool prefetch, int wave, const int (&va)[S::A_IPW],
@@ -113,12 +113,14 @@ __device__ __forceinline__ void k_step(f32x16 (&acc)[S::MB][S::NB], const GemmAr
   if (prefetch) {
     const int kb = (kt + 1) * kRowB;
     copy_tile<S::A_IPW>(Ab + kb, a_rows_bytes - kb, an, wave * S::A_IPW * 8, va);
-    copy_tile<S::B_IPW>(Wb + kb, S::TN * p.K * 2 - kb, bn, wave * S::B_IPW * 8, vb);
+    copy_tile<S::B_IPW>(Wb + kb, b_rows_bytes - kb, bn, wave * S::B_IPW * 8, vb);
   }
   mma_step<S>(acc, as, bs, fa, fb);
 }
 
-template <class S>
+// GLU: the tile's TN W rows are TN/2 gate rows and the matching TN/2 up rows
+// (N rows further), so the workgroup produces TN/2 gated output columns.
+template <class S, bool GLU>
 __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs p) {
   __shared__ __attribute__((aligned(1024))) unsigned char a_lds0[S::ATILE];
   __shared__ __attribute__((aligned(1024))) unsigned char b_lds0[S::BTILE];
@@ -140,12 +142,15 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, half = lane >> 5;
   const int wm = wave % S::WAVES_M, wn = wave / S::WAVES_M;
   const int64_t m0 = (int64_t)tm * S::TM;
-  const int n0 = tn * S::TN;
+  constexpr int OUT_TN = GLU ? S::TN / 2 : S::TN;  // output columns per tile
+  const int n0 = tn * OUT_TN;
   const int row_bytes = p.K * 2;
   const int rows_valid = (int)min((int64_t)S::TM, p.M - m0);
   const unsigned char *Ab = static_cast<const unsigned char *>(p.A) + m0 * row_bytes;
   const unsigned char *Wb = static_cast<const unsigned char *>(p.W) + (int64_t)n0 * row_bytes;
   const int a_rows_bytes = rows_valid * row_bytes;  // A rows past M read as zero
+  // W rows the tile reaches from Wb: TN, or up to the last up row in GLU mode
+  const int b_rows_bytes = (GLU ? p.N + S::TN / 2 : S::TN) * row_bytes;
 
   int va[S::A_IPW], vb[S::B_IPW];
 #pragma unroll
@@ -156,7 +161,8 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
 #pragma unroll
   for (int i = 0; i < S::B_IPW; ++i) {
     const int r = (wave * S::B_IPW + i) * 8 + lane / 8;
-    vb[i] = r * row_bytes + (((lane & 7) ^ swz(r)) << 4);
+    const int g = GLU && r >= S::TN / 2 ? p.N + r - S::TN / 2 : r;  // W row relative to Wb
+    vb[i] = g * row_bytes + (((lane & 7) ^ swz(r)) << 4);
   }
   int fa[S::MB][4], fb[S::NB][4];
 #pragma unroll
@@ -181,12 +187,13 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
 
   const int KT = p.K / kTK;
   copy_tile<S::A_IPW>(Ab, a_rows_bytes, a_lds0, wave * S::A_IPW * 8, va);
-  copy_tile<S::B_IPW>(Wb, S::TN * row_bytes, b_lds0, wave * S::B_IPW * 8, vb);
+  copy_tile<S::B_IPW>(Wb, b_rows_bytes, b_lds0, wave * S::B_IPW * 8, vb);
   for (int kt = 0; kt < KT; kt += 2) {
-    k_step<S>(acc, p, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < KT, wave, va, vb, fa, fb);
+    k_step<S>(acc, b_rows_bytes, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < KT, wave, va,
+              vb, fa, fb);
     if (kt + 1 < KT)
-      k_step<S>(acc, p, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < KT, wave, va, vb, fa,
-                fb);
+      k_step<S>(acc, b_rows_bytes, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < KT, wave,
+                va, vb, fa, fb);
   }
 
   // ---- epilogue -------------------------------------------------------------------
@@ -194,19 +201,26 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
   // tile buffers become staging space, STAGE_B bytes per wave (fp32 rows of
   // 256 B, 16-byte chunks XOR-swizzled by row), PASS_ROWS rows per pass
   __syncthreads();
-  unsigned char *stg;
-  {
-    const int off = wave * S::STAGE_B;  // the buffers are laid out back to back in this order
+  // wave w's region: bytes [w STAGE_B, (w+1) STAGE_B) of a_lds0 | b_lds0 |
+  // a_lds1 | b_lds1 taken in this order (a region never straddles two)
+  auto stage_of = [&](int w) -> unsigned char * {
+    const int off = w * S::STAGE_B;
     constexpr int A = S::ATILE, B = S::BTILE;
-    stg = off < A ? a_lds0 + off : off < A + B ? b_lds0 + (off - A) : off < 2 * A + B ? a_lds1 + (off - A - B)
+    return off < A ? a_lds0 + off : off < A + B ? b_lds0 + (off - A) : off < 2 * A + B ? a_lds1 + (off - A - B)
                                                                                        : b_lds1 + (off - 2 * A - B);
-  }
+  };
+  unsigned char *stg = stage_of(wave);
+  constexpr int WAVES_N = S::TN / S::WN;
+  // GLU: the gate waves (wn < WAVES_N / 2) finish the rows; their partner
+  // holds the up block of the same output columns
+  const bool finisher = !GLU || wn < WAVES_N / 2;
+  const unsigned char *stg_up = GLU ? stage_of(wave + S::WAVES_M * (WAVES_N / 2)) : stg;
   const int cg = lane & 7;
   const int n = n0 + wn * S::WN + cg * 8;
   float bias[8];
   {
     bf16x8 bv = bf16x8{};
-    if (p.bias) bv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.bias) + n);
+    if (!GLU && p.bias) bv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.bias) + n);
 #pragma unroll
     for (int e = 0; e < 8; ++e) bias[e] = (float)bv[e];
   }
@@ -227,15 +241,25 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
           *reinterpret_cast<f32x4 *>(stg + row * 256 + ((c ^ (row & 15)) << 4)) = v;
         }
     }
+    if (GLU) __syncthreads();  // the partner's up block is staged
     // each lane then finishes 8 consecutive columns of one row: 8 rows per round
 #pragma unroll
     for (int it = 0; it < S::PASS_ROWS / 8; ++it) {
+      if (!finisher) break;
       const int row = it * 8 + (lane >> 3);
       const int64_t m = m0 + wm * S::WM + pass * S::PASS_ROWS + row;
       const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg) ^ (row & 15)) << 4));
       const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg + 1) ^ (row & 15)) << 4));
       if (m < p.M) {
         float o[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        if (GLU) {
+          const f32x4 u0 = *reinterpret_cast<const f32x4 *>(stg_up + row * 256 + (((2 * cg) ^ (row & 15)) << 4));
+          const f32x4 u1 =
+              *reinterpret_cast<const f32x4 *>(stg_up + row * 256 + (((2 * cg + 1) ^ (row & 15)) << 4));
+          const float u[8] = {u0[0], u0[1], u0[2], u0[3], u1[0], u1[1], u1[2], u1[3]};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = o[e] / (1.0f + __expf(-o[e])) * u[e];
+        }
         if (p.residual) {
           const bf16x8 rv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.residual) + m * p.N + n);
 #pragma unroll
@@ -247,6 +271,7 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
         *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(p.C) + m * p.N + n) = out;
       }
     }
+    if (GLU) __syncthreads();  // the next pass restages over these rows
   }
 }
 
@@ -256,20 +281,23 @@ using LargeTile = Shape<256, 256, 128, 64>;  // 8 waves, one workgroup per CU
 template <class S>
 hipError_t launch_shape(GemmArgs p, hipStream_t st) {
   p.tiles_m = (int)((p.M + S::TM - 1) / S::TM);
-  p.tiles_n = p.N / S::TN;
+  p.tiles_n = p.N / (p.glu ? S::TN / 2 : S::TN);
   const int n_tiles = p.tiles_m * p.tiles_n;
   if (n_tiles <= 0) return hipSuccess;
   const int per_xcd = (n_tiles + kXcds - 1) / kXcds;
-  gemm_bf16_kernel<S><<<dim3(kXcds * per_xcd), dim3(S::THREADS), 0, st>>>(p);
+  if (p.glu) gemm_bf16_kernel<S, true><<<dim3(kXcds * per_xcd), dim3(S::THREADS), 0, st>>>(p);
+  else gemm_bf16_kernel<S, false><<<dim3(kXcds * per_xcd), dim3(S::THREADS), 0, st>>>(p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t st) {
-  // the large tile needs N % 256 == 0 and enough tiles to fill the CUs
-  const int64_t large_tiles = ((a.M + 255) / 256) * (a.N / 256);
-  if (a.N % 256 == 0 && large_tiles >= 2 * 256) return launch_shape<LargeTile>(a, st);
+  // the large tile needs whole output tiles (256 columns, 128 gated) and
+  // enough tiles to fill the CUs
+  const int out_tn = a.glu ? LargeTile::TN / 2 : LargeTile::TN;
+  const int64_t large_tiles = ((a.M + LargeTile::TM - 1) / LargeTile::TM) * (a.N / out_tn);
+  if (a.N % out_tn == 0 && large_tiles >= 2 * 256) return launch_shape<LargeTile>(a, st);
   return launch_shape<SmallTile>(a, st);
 }
 

@@ -184,6 +184,10 @@ def test_linear_and_row_op_checks():
     assert _status(daf.daf_linear, 10, 128, 64, None, FAKE, None, None, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
     assert _status(daf.daf_linear, 10, 128, 64, FAKE, FAKE, FAKE + 2, None, FAKE, 0) == daf.DAF_ERR_ALIGNMENT
     daf.daf_linear(0, 128, 64, None, None, None, None, None, 0)  # no rows: nothing to do
+    assert _status(daf.daf_linear_swiglu, 10, 96, 64, FAKE, FAKE, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+    assert _status(daf.daf_linear_swiglu, 10, 128, 100, FAKE, FAKE, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
+    assert _status(daf.daf_linear_swiglu, 10, 128, 64, FAKE, None, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
+    daf.daf_linear_swiglu(0, 128, 64, None, None, None, 0)
     assert _status(daf.daf_rmsnorm, 4, 12, FAKE, FAKE, 1e-6, FAKE, 0) == daf.DAF_ERR_UNSUPPORTED
     assert _status(daf.daf_rmsnorm, 4, 16, FAKE, FAKE, -1.0, FAKE, 0) == daf.DAF_ERR_INVALID_ARG
     daf.daf_rmsnorm(0, 16, None, None, 1e-6, None, 0)

@@ -188,3 +188,22 @@ def test_decoder_layer_full():
                                dec.full_attention(oracle_get(), 1.0 / np.sqrt(model.d)),
                                model.eps, model.theta, model.hq, model.hkv, model.d)
     _layer_close(_f(xa), ref, "full layer")
+
+
+@pytest.mark.parametrize("M,I,K", [(300, 192, 256), (5043, 18944, 3584), (1100, 14848, 512)])
+def test_linear_swiglu(M, I, K):
+    """Gate and up projections with SiLU(gate) * up in the epilogue; the last
+    two shapes take the 256 x 256 tile (128 gated columns per tile), oracle on
+    sampled rows."""
+    import paper_2607_21599_amd as daf
+    A, Wgu, _, _ = di.make_linear_case(M, 2 * I, K, seed=M + I, bias=False, residual=False)
+    C = torch.full((M + 3, I), 5.0, dtype=torch.bfloat16, device="cuda")
+    daf.daf_linear_swiglu(M, I, K, _dev(A), _dev(Wgu), C)
+    torch.cuda.synchronize()
+    rows = np.arange(M) if M <= 300 else np.union1d(
+        np.random.Generator(np.random.PCG64(2)).choice(M, 20, replace=False), [0, 255, 256, M - 1])
+    w = di.raw_to_f32
+    Wf = w(Wgu)
+    ref = dec.silu_mul(dec.linear(w(A[rows]), Wf[:I]), dec.linear(w(A[rows]), Wf[I:]))
+    _close(_f(C[torch.from_numpy(rows).cuda()]), ref, f"swiglu {M}x{I}x{K}")
+    assert torch.all(C[M:] == 5.0), "rows past M were written"
