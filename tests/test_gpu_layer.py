@@ -207,3 +207,61 @@ def test_linear_swiglu(M, I, K):
     ref = dec.silu_mul(dec.linear(w(A[rows]), Wf[:I]), dec.linear(w(A[rows]), Wf[I:]))
     _close(_f(C[torch.from_numpy(rows).cuda()]), ref, f"swiglu {M}x{I}x{K}")
     assert torch.all(C[M:] == 5.0), "rows past M were written"
+
+
+def test_decoder_layer_batch():
+    """A ragged batch of three requests (one without important tokens, one
+    without a question) in both modes; the oracle runs each request on its
+    own rows (the projections are row-independent)."""
+    import paper_2607_21599_amd as daf
+    from oracle import get as oracle_get
+    model = di.TINY_MODEL
+    reqs = [(300, 16, 45), (200, 9, 0), (500, 0, 75)]  # (L_d, L_q, n)
+    rng = np.random.Generator(np.random.PCG64(77))
+    bits, f = di.f32_to_bf16_bits, di.raw_to_f32
+    wts = di.make_layer_weights(model, 78)
+    w = _weights_on_gpu(model, wts)
+    ow = _oracle_weights(wts)
+    cfg = daf.AttnCfg(model.hq, model.hkv, model.d, daf.DAF_BF16)
+    cu_doc = np.cumsum([0] + [r[0] for r in reqs])
+    cu_q = np.cumsum([0] + [r[1] for r in reqs])
+    cu_imp = np.cumsum([0] + [r[2] for r in reqs])
+    batch = daf.Batch(cu_doc, cu_q, cu_imp)
+    xs, caches, idxs = [], [], []
+    for L_d, L_q, n in reqs:
+        xs.append(bits(rng.standard_normal((L_d + L_q, model.hidden), dtype=np.float32)))
+        caches.append(bits(rng.standard_normal((2, L_d + L_q, model.hkv, model.d), dtype=np.float32) * 0.5))
+        idxs.append(np.sort(rng.choice(L_d, n, replace=False)).astype(np.int32) if n else np.zeros(0, np.int32))
+    orc, sc = oracle_get(), 1.0 / np.sqrt(model.d)
+    run = lambda x, pos, attn: dec.decoder_layer(x, pos, ow, attn, model.eps, model.theta,  # noqa: E731
+                                                  model.hq, model.hkv, model.d)[0]
+    # DAF mode: every request's important rows, then every request's question rows
+    imp_x = np.concatenate([x[i] for x, i in zip(xs, idxs)])
+    q_x = np.concatenate([x[L_d:] for x, (L_d, _, _) in zip(xs, reqs)])
+    imp_pos = np.concatenate(idxs)
+    q_pos = np.concatenate([np.arange(L_d, L_d + L_q) for L_d, L_q, _ in reqs]).astype(np.int32)
+    xa = _dev(np.concatenate([imp_x, q_x]))
+    kc = _dev(np.concatenate([c[0] for c in caches]))
+    vc = _dev(np.concatenate([c[1] for c in caches]))
+    ws_bytes = daf.daf_decoder_layer_workspace_size(cfg, w, batch, daf.DAF_LAYER_DAF)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    daf.daf_decoder_layer(cfg, w, batch, daf.DAF_LAYER_DAF, _dev(np.concatenate(idxs)),
+                          _dev(np.concatenate([imp_pos, q_pos]).astype(np.int32)), xa, kc, vc, ws, ws_bytes)
+    # full mode on the same batch: every row of every request
+    xf = _dev(np.concatenate(xs))
+    posf = np.concatenate([np.arange(L_d + L_q) for L_d, L_q, _ in reqs]).astype(np.int32)
+    ws_f = daf.daf_decoder_layer_workspace_size(cfg, w, batch, daf.DAF_LAYER_FULL)
+    wsf = torch.empty(ws_f, dtype=torch.uint8, device="cuda")
+    daf.daf_decoder_layer(cfg, w, batch, daf.DAF_LAYER_FULL, None, _dev(posf), xf, None, None, wsf, ws_f)
+    torch.cuda.synchronize()
+    got_d, got_f = _f(xa), _f(xf)
+    ni = len(imp_x)
+    for b, (L_d, L_q, n) in enumerate(reqs):
+        rows = np.concatenate([idxs[b], np.arange(L_d, L_d + L_q)]).astype(np.int64)
+        ref = run(f(xs[b][rows]), rows, dec.daf_attention(orc, idxs[b], f(caches[b][0]), f(caches[b][1]), L_d, sc))
+        got = np.concatenate([got_d[cu_imp[b]:cu_imp[b + 1]], got_d[ni + cu_q[b]:ni + cu_q[b + 1]]])
+        if len(rows):
+            _layer_close(got, ref, f"DAF batch request {b}")
+        reff = run(f(xs[b]), np.arange(L_d + L_q), dec.full_attention(orc, sc))
+        t0 = cu_doc[b] + cu_q[b]
+        _layer_close(got_f[t0:t0 + L_d + L_q], reff, f"full batch request {b}")
