@@ -39,9 +39,25 @@ PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_stage1_qwen7b_32k_pmc.md")
 # sources whose change invalidates counter-measured traffic of the attention kernels
-ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_21599_amd", "csrc", f)
-                for f in ("attn_bf16.hip", "attn.hip", "api.hip", "daf_internal.h")] + [
+# What determines a standalone stage-1 launch: the kernel and its grid, the
+# launch structures, the compile flags, and the host functions that build the
+# stage-1 work table. A traffic record taken on other versions of these is not
+# used.
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_21599_amd", "csrc", f) for f in ("attn_bf16.hip", "daf_internal.h")] + [
     os.path.join(ROOT, "paper_2607_21599_amd", "build.py")]
+ATTN_HOST = os.path.join(ROOT, "paper_2607_21599_amd", "csrc", "api.hip")
+ATTN_HOST_FUNCTIONS = ("AttnEntry self_entry(", "int entry_groups(", "daf_status_t run_entries(",
+                       "void add_self_entries(")
+
+
+def _function_text(src: str, head: str) -> str:
+    """The text of the function that starts with `head` up to its closing
+    brace at the start of a line."""
+    i = src.find(head)
+    if i < 0:
+        return ""
+    j = src.find("\n}\n", i)
+    return src[i:j + 3]
 
 
 def attn_source_hash() -> str:
@@ -50,6 +66,10 @@ def attn_source_hash() -> str:
     for f in ATTN_SOURCES:
         with open(f, "rb") as fh:
             h.update(fh.read())
+    with open(ATTN_HOST) as fh:
+        src = fh.read()
+    for head in ATTN_HOST_FUNCTIONS:
+        h.update(_function_text(src, head).encode())
     return h.hexdigest()
 
 
