@@ -19,14 +19,25 @@
 //    operand (8 consecutive keys of one feature per lane) is read from the
 //    row-major V tile with ds_read_b64_tr_b16, which transposes 16-bit data
 //    across each 16-lane group.
-//  * Online softmax in fp32, base 2. Full tiles keep the running max per
-//    32-key half, so the S MFMAs of half 1 overlap the softmax of half 0 and
-//    the P.V MFMAs of half 0 overlap the max of half 1; diagonal tiles take one
-//    max over the tile. The running max is only raised when a row's max grows
-//    by more than 2^8 (probabilities stay <= 256, exact in fp32 and bf16
-//    range), so the O rescale is almost always skipped; the row max of a lane
+//  * Online softmax in fp32, base 2, scale folded into one FMA per score. Full
+//    tiles form each 32-key half's probabilities against the running max as it
+//    stands, without taking the half's max: only when some lane's share of the
+//    half's sum exceeds 2^32 (or is not finite, as on a row's first tile) is
+//    the half's exact max taken, the running max raised, O and the sum rescaled
+//    and the half formed again. Probabilities thus stay below 2^32 (far from
+//    overflow in fp32 and bf16) and the S MFMAs of half 1 run beside the
+//    softmax of half 0. Diagonal tiles take one max over the tile and raise the
+//    running max only when it grows by more than 2^8. The row max of a lane
 //    pair is exchanged with v_permlane32_swap.
+//  * The row sum is taken from the bf16-rounded probabilities that the P.V
+//    product uses (v_dot2c_f32_bf16 against (1, 1), one instruction per pair).
+//  * Launch shape for causal self attention: the heaviest 128 jobs of an XCD
+//    (one query head of one 128-row block each) are run by its 64 resident
+//    workgroups in pairs, job u with job 127 - u, so each workgroup gets a heavy
+//    and a light block of near-equal total; lighter jobs get a workgroup each.
 #include <math.h>
+
+#include <algorithm>
 
 #include "daf_internal.h"
 
@@ -35,6 +46,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
@@ -45,6 +57,12 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 constexpr int kBN = 64;                  // keys per tile
 constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may grow before O is rescaled
+// Full tiles skip the max: a half's probabilities are formed with the running
+// max as it stands, and only if some lane's share of the half's sum exceeds
+// this (or is not finite) is the half's exact max taken, the running max
+// raised and the half formed again. Each probability is then at most 2^32, far
+// from fp32 and bf16 overflow in the row sum and the O accumulators.
+constexpr float kHalfSumLimit = 4294967296.0f;
 
 template <int D>
 struct Geo {
@@ -162,17 +180,22 @@ struct WaveState {
   float sl2;
 };
 
-// P^T operands (bf16) of one 32-key half and the running row-sum update.
+// P^T operands (bf16) of one 32-key half; returns this lane's share of the
+// half's row sum, taken from the rounded probabilities that the P.V product
+// uses (pairs summed by v_dot2c_f32_bf16 against (1, 1)).
 template <int D>
-__device__ __forceinline__ void softmax_half(WaveState<D> &w, const f32x16 &sacc, float m_use, bf16x8 (&pf)[2]) {
-  float ps[4] = {0.f, 0.f, 0.f, 0.f};
+__device__ __forceinline__ float softmax_half(const WaveState<D> &w, const f32x16 &sacc, float m_use,
+                                              bf16x8 (&pf)[2]) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float e = fast_exp2(__builtin_fmaf(sacc[r], w.sl2, -m_use));
-    ps[r & 3] += e;
-    pf[r >> 3][r & 7] = (__bf16)e;
+  for (int r = 0; r < 16; ++r) pf[r >> 3][r & 7] = (__bf16)fast_exp2(__builtin_fmaf(sacc[r], w.sl2, -m_use));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float ps[2] = {0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const bf16x2 pr = {pf[j >> 2][2 * (j & 3)], pf[j >> 2][2 * (j & 3) + 1]};
+    ps[j & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ps[j & 1], false);
   }
-  w.l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  return ps[0] + ps[1];
 }
 
 // O^T += V^T P^T over the 2 x 16 keys of one half tile.
@@ -194,15 +217,17 @@ __device__ __forceinline__ void pv_half(WaveState<D> &w, const unsigned char *vs
 // Raise the running max if this half's max grew by more than the slack
 // (wave-uniform decision), rescaling O and the row sum.
 template <int D>
-__device__ __forceinline__ void maybe_raise(WaveState<D> &w, float mt) {
-  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) {
-    const float m_new = fmaxf(w.m_run, mt);
-    const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
-    w.m_run = m_new;
-    w.l_run *= alpha;
+__device__ __forceinline__ void raise_to(WaveState<D> &w, float mt) {
+  const float m_new = fmaxf(w.m_run, mt);
+  const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(w.m_run - m_new);
+  w.m_run = m_new;
+  w.l_run *= alpha;
 #pragma unroll
-    for (int db = 0; db < Geo<D>::DB; ++db) w.oacc[db] *= alpha;
-  }
+  for (int db = 0; db < Geo<D>::DB; ++db) w.oacc[db] *= alpha;
+}
+template <int D>
+__device__ __forceinline__ void maybe_raise(WaveState<D> &w, float mt) {
+  if (__builtin_amdgcn_ballot_w64(mt > w.m_run + kRescaleSlack) != 0) raise_to<D>(w, mt);
 }
 template <int D>
 __device__ __forceinline__ float half_max(const WaveState<D> &w, const f32x16 &sacc) {
@@ -226,24 +251,40 @@ __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *
     for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) kf[b2][ds] = *reinterpret_cast<const bf16x8 *>(ks + b2 * 32 * ROWB + w.koff[ds]);
-    f32x16 s0 = f32x16{};
+    f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0][ds], w.qf[ds], s0, 0, 0, 0);
-    const float mt0 = half_max<D>(w, s0);
-    // scheduling hint: all K reads first, then the S MFMAs of half 0
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * DS, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, DS, 0);
-    maybe_raise<D>(w, mt0);
-    f32x16 s1 = f32x16{};
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[1][ds], w.qf[ds], s1, 0, 0, 0);
     bf16x8 pf0[2];
-    softmax_half<D>(w, s0, w.m_run, pf0);
+    float ps0 = softmax_half<D>(w, s0, w.m_run, pf0);
+    // scheduling: K reads of half 0, the S MFMAs of half 0 each beside a K
+    // read of half 1, then the S MFMAs of half 1 each beside a sixth of the
+    // softmax of half 0
+    __builtin_amdgcn_sched_group_barrier(0x100, DS, 0);
+#pragma unroll
+    for (int i = 0; i < DS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < DS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+    }
+    if (__builtin_amdgcn_ballot_w64(!(ps0 <= kHalfSumLimit)) != 0) {
+      raise_to<D>(w, half_max<D>(w, s0));
+      ps0 = softmax_half<D>(w, s0, w.m_run, pf0);
+    }
+    w.l_run += ps0;
     pv_half<D>(w, vs, pf0);
-    const float mt1 = half_max<D>(w, s1);
-    maybe_raise<D>(w, mt1);
     bf16x8 pf1[2];
-    softmax_half<D>(w, s1, w.m_run, pf1);
+    float ps1 = softmax_half<D>(w, s1, w.m_run, pf1);
+    if (__builtin_amdgcn_ballot_w64(!(ps1 <= kHalfSumLimit)) != 0) {
+      raise_to<D>(w, half_max<D>(w, s1));
+      ps1 = softmax_half<D>(w, s1, w.m_run, pf1);
+    }
+    w.l_run += ps1;
     pv_half<D>(w, vs + 32 * ROWB, pf1);
     return;
   }
@@ -276,10 +317,10 @@ __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *
   maybe_raise<D>(w, pair_max(mx) * w.sl2);
   const float m_use = (w.m_run == -INFINITY) ? 0.f : w.m_run;
   bf16x8 pf0[2], pf1[2];
-  softmax_half<D>(w, sacc[0], m_use, pf0);
+  w.l_run += softmax_half<D>(w, sacc[0], m_use, pf0);
   pv_half<D>(w, vs, pf0);
   if (second) {
-    softmax_half<D>(w, sacc[1], m_use, pf1);
+    w.l_run += softmax_half<D>(w, sacc[1], m_use, pf1);
     pv_half<D>(w, vs + 32 * ROWB, pf1);
   }
 }
@@ -302,18 +343,14 @@ __device__ __forceinline__ void tile_step(WaveState<D> &w, const unsigned char *
   else tile_math<D, false>(w, ks, vs, kb);
 }
 
+// One job: the work of launch slot `slot` of XCD `xcd` (one query head of one
+// work group, or one packed stage-2 unit group), run by the whole workgroup.
 template <int D, int KIND>
-__global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLaunch p) {
+__device__ __forceinline__ void attn_job(const AttnLaunch &p, const int xcd, const int slot, unsigned char *k_lds0,
+                                         unsigned char *v_lds0, unsigned char *k_lds1, unsigned char *v_lds1) {
   using Gm = Geo<D>;
   constexpr int ROWB = Gm::ROWB, CH = Gm::CH, TILE = Gm::TILE, IPW = Gm::IPW, DS = Gm::DS, DB = Gm::DB;
   constexpr int RPI = Gm::RPI;
-  // separate objects per stage and tensor: lets the compiler see that the DMA
-  // into one buffer does not alias reads of another
-  __shared__ __attribute__((aligned(1024))) unsigned char k_lds0[TILE];
-  __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
-  __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
-  __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
-
   // ---- which work -----------------------------------------------------------
   // A work group is the G heads that share one KV head, for one entry, query
   // block and key split. When Hkv divides the 8 XCDs, each XCD serves one KV
@@ -323,8 +360,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   // work groups run heaviest first, and the G heads of a work group are
   // consecutive workgroups of that XCD.
   const int G = p.group, WPG = p.wgs_per_group;
-  const int xcd = blockIdx.x % kXcds;
-  const int slot = blockIdx.x / kXcds;
   const int hl = slot % WPG;
   int g, lam;  // KV head, index of the work group among that head's work groups
   if (kXcds % p.hkv == 0) {
@@ -490,8 +525,35 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLa
   }
 }
 
+// Launch shape: the first pair_wgs workgroups of each XCD each run two jobs,
+// slot u and slot 2*pair_wgs-1-u of the XCD's heaviest-first list (a heavy job
+// with a light one, so that their sums are nearly equal), and every further
+// workgroup runs one of the remaining, lightest slots. With pair_wgs = 0 each
+// workgroup runs one slot.
+template <int D, int KIND>
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_bf16_kernel(const AttnLaunch p) {
+  constexpr int TILE = Geo<D>::TILE;
+  // separate objects per stage and tensor: lets the compiler see that the DMA
+  // into one buffer does not alias reads of another
+  __shared__ __attribute__((aligned(1024))) unsigned char k_lds0[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char v_lds0[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char k_lds1[TILE];
+  __shared__ __attribute__((aligned(1024))) unsigned char v_lds1[TILE];
+  const int xcd = blockIdx.x % kXcds;
+  const int u = blockIdx.x / kXcds;
+  const bool paired = u < p.pair_wgs;
+  const int first = paired ? u : u + p.pair_wgs;
+  const int second = 2 * p.pair_wgs - 1 - u;
+  const int n_jobs = (paired && second < p.slots_per_xcd) ? 2 : 1;
+  for (int j = 0; j < n_jobs; ++j) {
+    if (j) __syncthreads();  // every wave is done with the LDS buffers of the first job
+    attn_job<D, KIND>(p, xcd, j ? second : first, k_lds0, v_lds0, k_lds1, v_lds1);
+  }
+}
+
 template <int D>
-hipError_t launch_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
+hipError_t launch_t(AttnKind kind, const AttnLaunch &p0, hipStream_t st) {
+  AttnLaunch p = p0;
   // slots per XCD: work groups per XCD times the G heads of a work group
   int per_xcd;
   if (kXcds % p.hkv == 0) {
@@ -501,7 +563,19 @@ hipError_t launch_t(AttnKind kind, const AttnLaunch &p, hipStream_t st) {
     per_xcd = (p.n_groups + kXcds - 1) / kXcds;
   }
   const int slots = p.wgs_per_group * per_xcd;
-  const dim3 grid(kXcds * slots), block(kAttnThreads);
+  // Causal self attention: the heaviest 2 * kResidentPerXcd slots of an XCD
+  // run in heavy/light pairs (see the kernel). Slots are in heaviest-first
+  // order within an entry, and entries heaviest request first, so the pairing
+  // is used when the first entry alone fills those slots.
+  const int xph = kXcds % p.hkv == 0 ? kXcds / p.hkv : 0;
+  const int first_groups = xph ? p.e[0].mb_count / xph : p.e[0].mb_count * p.hkv / kXcds;
+  p.slots_per_xcd = slots;
+  p.pair_wgs = (kind == AttnKind::kSelf && p.e[0].n_splits == 1 &&
+                first_groups * p.wgs_per_group >= 2 * kResidentPerXcd)
+                   ? kResidentPerXcd
+                   : 0;
+  const int wgs = p.pair_wgs ? p.pair_wgs + std::max(0, slots - 2 * p.pair_wgs) : slots;
+  const dim3 grid(kXcds * wgs), block(kAttnThreads);
   switch (kind) {
     case AttnKind::kSelf: attn_bf16_kernel<D, 0><<<grid, block, 0, st>>>(p); break;
     default: attn_bf16_kernel<D, 1><<<grid, block, 0, st>>>(p); break;

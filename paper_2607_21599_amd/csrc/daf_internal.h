@@ -13,6 +13,7 @@ constexpr int kAttnBM = 128;      // query rows per attention workgroup
 constexpr int kMaxEntries = 32;   // work-table entries per attention launch (kernel argument < 4 KiB)
 constexpr int kMaxRowReqs = 32;   // requests per row-movement launch
 constexpr int kTargetWorkgroups = 512;  // 256 CUs x 2 resident attention workgroups
+constexpr int kResidentPerXcd = 64;     // resident attention workgroups per XCD (32 CUs x 2)
 
 // One entry of an attention launch: one request of one stage, restricted to a
 // contiguous range of 128-row query blocks. Query row i (0-based in the
@@ -65,6 +66,10 @@ struct AttnLaunch {
   int32_t n_entries;
   int32_t n_groups;        // total work groups over all entries
   float scale_log2;        // softmax scale * log2(e)
+  // launch shape, set by the launcher: slots per XCD, and the number of
+  // workgroups per XCD that run two slots (a heavy and a light one; 0 = none)
+  int32_t slots_per_xcd;
+  int32_t pair_wgs;
   AttnEntry e[kMaxEntries];
 };
 
