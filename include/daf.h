@@ -45,7 +45,11 @@
  *   question tokens 0..j.
  * Numerics. bf16 or fp32 in; fp32 accumulation and softmax; outputs in the
  *   input dtype. bf16 attention rounds the softmax probabilities to bf16
- *   before the value product.
+ *   before the value product and normalises by the sum of those rounded
+ *   probabilities, so each output row is a weighted mean of value rows with
+ *   weights that sum to one; its LSE is the log of that same sum, within
+ *   ln(1 + 2^-8) of the exact log-sum-exp (the bf16 rounding of a term that
+ *   dominates its row).
  * Asynchrony. Work is enqueued on `stream` (NULL = the default stream) and the
  *   call returns without synchronising. There is no global state: calls are
  *   re-entrant; calls that write the same buffers must be ordered by the

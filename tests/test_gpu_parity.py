@@ -317,6 +317,51 @@ def test_peaked_softmax():
     assert_attn_close(_f32(buf["o_q"]), ref["o_q"], di.BF16, "peaked stage2")
 
 
+def test_running_max_raised_late():
+    """Keys whose logits jump far above every earlier one (by ~40 in log2
+    units per step), placed well below the diagonal: the kernel forms a full
+    tile's probabilities against the running max as it stands and must catch
+    the overflow, raise the max, rescale and form the tile again, in stage 1
+    and in stage 2 (where the loud keys reach the hybrid cache through the
+    important rows, plus one offline cache row). A last key ~10 units above
+    the max is formed against the old max (probability ~2^10, bf16-rounded),
+    which the LSE bar covers."""
+    shape = _shape("loud_keys", 3000, 40, 900, hq=8, hkv=2, d=128, seed=41)
+    batch = di.make_batch([shape])
+    a = batch.arrays
+    d, hkv = shape.d, shape.hkv
+    u = np.full(d, 1.0 / np.sqrt(d), np.float32)
+    for k in ("q_imp", "q_q"):
+        q = di.raw_to_f32(a[k]) + np.float32(8.0) * u
+        a[k] = di.f32_to_bf16_bits(q)
+    k_imp, v_imp = di.raw_to_f32(a["k_imp"]), di.raw_to_f32(a["v_imp"])
+    # three keys each ~40 log2 units above the last (the max is raised), then
+    # one ~10 units above (formed against the old max: its probability ~2^10)
+    for j, (pos, beta) in enumerate(((100, 40.0), (300, 80.0), (500, 120.0), (700, 130.0))):
+        k_imp[pos] = np.float32(beta) * u
+        v_imp[pos] = np.float32(j + 1)
+    a["k_imp"], a["v_imp"] = di.f32_to_bf16_bits(k_imp), di.f32_to_bf16_bits(v_imp)
+    idx = a["idx"][: shape.n]
+    free = np.setdiff1d(np.arange(shape.L_d - 200), idx)
+    k_cache, v_cache = di.raw_to_f32(a["k_cache"]), di.raw_to_f32(a["v_cache"])
+    k_cache[free[-1]] = np.float32(160.0) * u
+    v_cache[free[-1]] = np.float32(4.0)
+    a["k_cache"], a["v_cache"] = di.f32_to_bf16_bits(k_cache), di.f32_to_bf16_bits(v_cache)
+    assert k_imp.shape[1:] == (hkv, d)
+    buf = _buffers(batch)
+    buf.layer()
+    torch.cuda.synchronize()
+    ref = oracle_request(batch.request(0))
+    assert_attn_close(_f32(buf["o_imp"]), ref["o_imp"], di.BF16, "loud keys stage1")
+    assert_attn_close(_f32(buf["o_q"]), ref["o_q"], di.BF16, "loud keys stage2")
+    assert_lse_close(_f32(buf["lse_imp"]).T, ref["lse_imp"], di.BF16, "loud keys stage1 lse")
+    assert_lse_close(_f32(buf["lse_q"]).T, ref["lse_q"], di.BF16, "loud keys stage2 lse")
+    # the loud keys dominate: each row returns the value of the loudest key it sees
+    o1 = _f32(buf["o_imp"])
+    assert np.allclose(o1[600:700], 3.0, atol=2e-2)
+    assert np.allclose(o1[704:], 4.0, atol=2e-2)
+
+
 def test_repeat_runs_bit_identical():
     batch = di.make_batch(di.workload("qwen7b_16k_r15"))
     buf = _buffers(batch)
