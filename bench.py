@@ -3,8 +3,10 @@
 One step is one pass of the whole hot path over one synthetic layer already
 resident in HBM: the important-row gather of the hidden states, then
 daf_layer_attn (hybrid KV write-back, stage 2 with its split merge, stage 1;
-both stages write their rows into the hidden states in their epilogues). W untimed warmup steps, then exactly K
-timed steps between device synchronisations. Several copies of the inputs are
+both stages write their rows into the hidden states in their epilogues). At
+least W untimed warmup steps (and at least --warmup-ms of GPU time, so that the
+shader clock has reached its level under sustained load), then exactly K timed
+steps between device synchronisations. Several copies of the inputs are
 used in rotation so that consecutive steps do not find their data in the
 256 MB Infinity Cache.
 
@@ -243,7 +245,10 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup-ms", type=float, default=100.0,
+                    help="keep running untimed warmup steps until at least this much GPU time has passed "
+                         "(the shader clock ramps up over the first ~10 ms of sustained load)")
     ap.add_argument("--workload", default="qwen7b_32k")
     ap.add_argument("--copies", type=int, default=3, help="input copies used in rotation")
     ap.add_argument("--cpu-stride1", type=int, default=4)
@@ -291,14 +296,25 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    # Untimed warmup: at least W steps and at least --warmup-ms of GPU time.
+    # Steps timed right after a short warmup run ~20% slower while the clocks
+    # ramp up under the sustained load.
+    w0 = torch.cuda.Event(enable_timing=True)
+    w1 = torch.cuda.Event(enable_timing=True)
+    warm_steps, warm_ms = 0, 0.0
+    w0.record()
+    while warm_steps < args.warmup or warm_ms < args.warmup_ms:
+        for _ in range(max(1, args.warmup - warm_steps) if warm_steps < args.warmup else 10):
+            step(warm_steps)
+            warm_steps += 1
+        w1.record()
+        torch.cuda.synchronize()
+        warm_ms = w0.elapsed_time(w1)
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record()
     for i in range(args.steps):
-        step(i)
+        step(warm_steps + i)
     t1.record()
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
@@ -459,7 +475,8 @@ def main():
 
     out = {
         "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
+        "warmup": args.warmup, "warmup_steps_run": warm_steps, "warmup_gpu_ms": round(warm_ms, 1),
+        "ms_per_step": ms_per_step, "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if s0.dtype == di.BF16 else "f32", "data": "synthetic",
         "config": {"workload": args.workload, "L_d": [s.L_d for s in shapes] if len(shapes) > 1 else s0.L_d,
                    "L_q": [s.L_q for s in shapes] if len(shapes) > 1 else s0.L_q,
