@@ -43,7 +43,6 @@ template <typename T> struct Vec;
 template <> struct Vec<__bf16> {
   using v8 = bf16x8;  // one MFMA operand per lane: 8 elements, 16 bytes
   using v4 = bf16x4;
-  static constexpr int kKeyTile = 64;
 };
 template <> struct Vec<float> {
   using v8 = f32x8;   // 8 elements, 32 bytes

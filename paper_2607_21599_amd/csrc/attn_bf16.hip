@@ -244,7 +244,7 @@ __device__ __forceinline__ float half_max(const WaveState<D> &w, const f32x16 &s
 // half 1.
 template <int D, bool MASK>
 __device__ __forceinline__ void tile_math(WaveState<D> &w, const unsigned char *ks, const unsigned char *vs, int kb) {
-  constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS, DB = Geo<D>::DB;
+  constexpr int ROWB = Geo<D>::ROWB, DS = Geo<D>::DS;
   if (!MASK) {
     bf16x8 kf[2][DS];
 #pragma unroll
