@@ -389,6 +389,39 @@ def main():
                     traffic=measured_traffic(args.workload), traffic_unit="bytes per launch (HBM, counters)",
                     flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
 
+    # Stage 2 in its bandwidth-bound regime: the same layer with a 32-token
+    # question (7 query rows per cached K/V byte, below the MFMA/HBM ridge),
+    # timed alone like the stage calls above, three input copies in rotation.
+    stage2_lq32 = None
+    if not args.no_patterns and args.workload == "qwen7b_32k":
+        print("[bench] stage 2 at L_q = 32", file=sys.stderr, flush=True)
+        shp32 = di.workload("qwen7b_32k_lq32")
+        b32 = di.make_batch(shp32)
+        bufs32 = [LayerBuffers(b32.arrays, b32.cu_doc, b32.cu_q, b32.cu_imp, s0.hq, s0.hkv, s0.d)
+                  for _ in range(max(1, args.copies))]
+        for bb in bufs32:
+            bb.fuse_kv()
+        bufs32[0].stage2()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for i in range(args.steps):
+            torch.cuda._sleep(spin_cycles)
+            ev[i][0].record()
+            bufs32[i % len(bufs32)].stage2()
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        us32 = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        wk32 = work(shp32)
+        t_hbm = wk32["stage2_bytes"] / (PEAK_HBM_GBS * 1e9)
+        t_mma = wk32["stage2_flop"] / (peak_mma * 1e12)
+        stage2_lq32 = {"workload": "qwen7b_32k_lq32", "L_q": shp32[0].L_q, "us": us32,
+                       "bytes": wk32["stage2_bytes"], "GBps": gbs(wk32["stage2_bytes"], us32),
+                       "hbm_frac": gbs(wk32["stage2_bytes"], us32) / PEAK_HBM_GBS,
+                       "flop": wk32["stage2_flop"], "TFLOPs": tflops(wk32["stage2_flop"], us32),
+                       "floor_us": {"hbm": t_hbm * 1e6, "mfma": t_mma * 1e6},
+                       "roofline_frac": max(t_hbm, t_mma) / (us32 * 1e-6)}
+        del bufs32, b32
+
     selection = None
     if not args.no_patterns:
         # The step before the path: choosing the important tokens from the KV
@@ -487,6 +520,8 @@ def main():
         "stages": stages,
         "roofline": roofline,
     }
+    if stage2_lq32 is not None:
+        out["stage2_lq32"] = stage2_lq32
     if selection is not None:
         out["selection"] = selection
     if comparison is not None:
