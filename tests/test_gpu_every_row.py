@@ -8,7 +8,8 @@ tests cannot do: a query block whose job never ran, ran twice into the wrong
 rows, or ran over the wrong key range shows up here. The layouts cover the
 ways the kernels deal their jobs: KV heads served by XCD pairs, by single
 XCDs, or dealt round-robin over the XCDs; one request and several; the
-heavy/light pairing of causal jobs on and off; head dims 128 and 64.
+heavy/light pairing of causal jobs on and off; head dims 128 and 64; and the
+comparison patterns (queries at given positions) at the benchmark's size.
 """
 from __future__ import annotations
 
@@ -86,3 +87,33 @@ def test_zero_queries_every_row(layout):
         hid = buf["hidden"][int(batch.cu_tok[b]):int(batch.cu_tok[b + 1])].float().cpu().numpy()
         assert np.array_equal(hid[r["idx"]].reshape(s.n, s.hq, s.d), o_imp[i0:i1]), f"{layout} req {b} hidden"
         assert np.array_equal(hid[s.L_d:].reshape(s.L_q, s.hq, s.d), o_q[q0:q1]), f"{layout} req {b} hidden q"
+
+
+def test_zero_queries_every_row_patterns_32k():
+    """The comparison patterns at the benchmark's size, every row: the
+    CacheBlend rows (important and question tokens at their positions over the
+    whole hybrid cache) and full recomputation (every token over its prefix)
+    return the mean of the cache's value rows up to their position."""
+    from paper_2607_21599_amd.tensors import LayerBuffers
+    s = LAYOUTS["xcd_pairs_32k"][0]
+    batch = di.make_batch([s])
+    a = batch.arrays
+    a["q_imp"] = np.zeros_like(a["q_imp"])
+    a["q_q"] = np.zeros_like(a["q_q"])
+    buf = LayerBuffers(a, batch.cu_doc, batch.cu_q, batch.cu_imp, s.hq, s.hkv, s.d)
+    buf.fuse_kv()
+    buf.prepare_patterns(np.zeros((s.T, s.hq, s.d), dtype=np.uint16))
+    buf.cacheblend()
+    buf.full_recompute()
+    torch.cuda.synchronize()
+    r = batch.request(0)
+    _, vh = orc_mod.get().hybrid_kv(r["k_cache"], r["v_cache"], r["idx"], r["k_imp"], r["v_imp"], r["k_q"],
+                                    r["v_q"], s.L_d)
+    means = _running_means(di.raw_to_f32(vh), s.hq)
+    pos = np.concatenate([r["idx"].astype(np.int64), s.L_d + np.arange(s.L_q)])
+    assert_attn_close(buf["o_cb"].float().cpu().numpy(), means[pos], di.BF16, "CacheBlend pattern")
+    assert_lse_close(buf["lse_cb"].cpu().numpy().T, np.log(pos + 1.0)[:, None].repeat(s.hq, axis=1), di.BF16,
+                     "CacheBlend pattern lse")
+    assert_attn_close(buf["o_full"].float().cpu().numpy(), means, di.BF16, "full recomputation")
+    assert_lse_close(buf["lse_full"].cpu().numpy().T, np.log(np.arange(1, s.T + 1.0))[:, None].repeat(s.hq, axis=1),
+                     di.BF16, "full recomputation lse")
