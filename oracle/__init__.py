@@ -10,8 +10,8 @@ the order the paper gives (Sec. 2):
 
   1. hybrid KV cache: the important tokens' recomputed K/V replace the offline
      rows before question-document attention (Sec. 2 item 2), and the
-     question's own K/V follow the documents (the key set covers "all preceding
-     documents and the question");
+     question's own K/V follow the documents (the question's keys are every
+     document token and the question's own tokens);
   2. stage 1, important-token self-attention over the condensed sequence
      (Sec. 2 item 1; important tokens see only each other, Complexity
      Analysis);
