@@ -493,7 +493,7 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
 // ---- decoder layer around the attention -------------------------------------
 struct LayerWs {
   int64_t rows;
-  size_t h, q, k, v, o, m, attn, attn_bytes, total;  // byte offsets, total size
+  size_t h, q, k, v, o, m, attn, attn_bytes, part, total;  // byte offsets, total size
 };
 
 daf_status_t check_weights(const Cfg &c, const daf_layer_weights_t *w) {
@@ -532,12 +532,14 @@ LayerWs layer_ws(const Cfg &c, const daf_layer_weights_t &w, const Batch &b, int
   l.m = take(r * w.inter * e);
   l.attn_bytes = mode == DAF_LAYER_DAF ? ws_layout(c, b, plan_splits(c, b)).total : 0;
   l.attn = take(l.attn_bytes);
+  l.part = take(kGemmPartBytes);  // fp32 k pieces of the projections' tail tiles
   l.total = off;
   return l;
 }
 
+// part: workspace for the k pieces of tail tiles (kGemmPartBytes), or null
 daf_status_t gemm(int64_t M, int N, int K, const void *A, const void *W, const void *bias, const void *res, void *C,
-                  hipStream_t st) {
+                  hipStream_t st, float *part = nullptr) {
   GemmArgs g{};
   g.A = A;
   g.W = W;
@@ -547,7 +549,7 @@ daf_status_t gemm(int64_t M, int N, int K, const void *A, const void *W, const v
   g.M = M;
   g.N = N;
   g.K = K;
-  const hipError_t e = launch_gemm(g, st);
+  const hipError_t e = part ? launch_gemm_split(g, part, kGemmPartBytes, st) : launch_gemm(g, st);
   return e == hipSuccess ? DAF_OK : hip_fail(e, "linear launch");
 }
 
@@ -867,9 +869,10 @@ daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weight
     const int H = w->hidden, I = w->inter, QW = c.hq * c.d, KW = c.hkv * c.d;
     const hipError_t e0 = launch_rmsnorm(R, H, x, w->w_in, w->eps, h, stream);
     if (e0 != hipSuccess) return hip_fail(e0, "rmsnorm launch");
-    CHECK(gemm(R, QW, H, h, w->wq, w->bq, nullptr, q, stream));
-    CHECK(gemm(R, KW, H, h, w->wk, w->bk, nullptr, k, stream));
-    CHECK(gemm(R, KW, H, h, w->wv, w->bv, nullptr, v, stream));
+    float *part = reinterpret_cast<float *>(ws + l.part);
+    CHECK(gemm(R, QW, H, h, w->wq, w->bq, nullptr, q, stream, part));
+    CHECK(gemm(R, KW, H, h, w->wk, w->bk, nullptr, k, stream, part));
+    CHECK(gemm(R, KW, H, h, w->wv, w->bv, nullptr, v, stream, part));
     hipError_t e1 = launch_rope(R, c.hq, c.d, QW, q, pos, w->rope_theta, stream);
     if (e1 == hipSuccess) e1 = launch_rope(R, c.hkv, c.d, KW, k, pos, w->rope_theta, stream);
     if (e1 != hipSuccess) return hip_fail(e1, "rope launch");
@@ -908,7 +911,7 @@ daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weight
       }
       CHECK(run_entries(c, AttnKind::kSelf, entries, stream));
     }
-    CHECK(gemm(R, H, QW, o, w->wo, nullptr, x, x, stream));
+    CHECK(gemm(R, H, QW, o, w->wo, nullptr, x, x, stream, part));
     const hipError_t e2 = launch_rmsnorm(R, H, x, w->w_post, w->eps, h, stream);
     if (e2 != hipSuccess) return hip_fail(e2, "rmsnorm launch");
     {  // gate and up projections with SiLU(gate) * up in the epilogue
@@ -923,7 +926,7 @@ daf_status_t daf_decoder_layer(const daf_attn_cfg_t *cfg, const daf_layer_weight
       const hipError_t e3 = launch_gemm(g, stream);
       if (e3 != hipSuccess) return hip_fail(e3, "linear launch");
     }
-    CHECK(gemm(R, H, I, m, w->wd, nullptr, x, x, stream));
+    CHECK(gemm(R, H, I, m, w->wd, nullptr, x, x, stream, part));
     return ok();
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");

@@ -173,8 +173,21 @@ struct GemmArgs {
   // SiLU((A W^T)[m][j]) * (A W^T)[m][N + j] (no bias or residual)
   int32_t glu;
   int32_t tiles_m, tiles_n;  // filled by launch_gemm
+  // launch_gemm_split only: output tiles t_begin .. t_begin + t_count - 1 of
+  // the tile order; with `part` set each tile's k range is cut into k_parts
+  // pieces whose fp32 sums go to part[(tile - t_begin) * k_parts + piece]
+  // ([TM][TN] each) instead of C
+  int32_t t_begin, t_count, k_parts;
+  float *part;
 };
 hipError_t launch_gemm(const GemmArgs &a, hipStream_t st);
+// The same product, with the output tiles that do not fill a whole round of
+// the resident workgroups cut along k over the idle slots: their fp32 pieces
+// go to `part` (at most part_bytes) and a reduction adds them, the bias and
+// the residual. Falls back to launch_gemm when that does not apply (gated
+// mode, too little workspace or k).
+hipError_t launch_gemm_split(const GemmArgs &a, float *part, size_t part_bytes, hipStream_t st);
+constexpr size_t kGemmPartBytes = (size_t)512 * 128 * 128 * 4;  // fp32 pieces of one round of small tiles
 hipError_t launch_rmsnorm(int64_t rows, int width, const void *x, const void *w, float eps, void *y,
                           hipStream_t st);
 hipError_t launch_rope(int64_t rows, int heads, int d, int64_t row_stride, void *x, const int32_t *pos,

@@ -18,6 +18,8 @@
 // Tile order: the tiles are split into 8 contiguous ranges, one per XCD
 // (workgroup i runs on XCD i mod 8); within a range, groups of 8 M-tiles sweep
 // the N-tiles, so the A rows of a group stay in that XCD's L2 while W streams.
+#include <algorithm>
+
 #include "daf_internal.h"
 
 namespace daf {
@@ -32,7 +34,7 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 constexpr int kTK = 64;                         // k step
 constexpr int kRowB = kTK * 2;                  // bytes per tile row in LDS
 constexpr int kGroupM = 8;                      // M-tiles per group of the tile order
-constexpr int kRsrcWord3 = 0x00020000;          // raw buffer descriptor word 3 (gfx9 family)
+[[maybe_unused]] constexpr int kRsrcWord3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
@@ -118,9 +120,19 @@ __device__ __forceinline__ void k_step(f32x16 (&acc)[S::MB][S::NB], int b_rows_b
   mma_step<S>(acc, as, bs, fa, fb);
 }
 
+// Output tile t of the tile order: groups of kGroupM M-tiles sweep the N-tiles.
+__device__ __forceinline__ void tile_coords(const GemmArgs &p, int t, int &tm, int &tn) {
+  const int span = kGroupM * p.tiles_n;
+  const int first_m = (t / span) * kGroupM;
+  const int gsize = min(p.tiles_m - first_m, kGroupM);
+  tm = first_m + (t % span) % gsize;
+  tn = (t % span) / gsize;
+}
+
 // GLU: the tile's TN W rows are TN/2 gate rows and the matching TN/2 up rows
 // (N rows further), so the workgroup produces TN/2 gated output columns.
-template <class S, bool GLU>
+// PARTIAL: one k piece of a tail tile, its fp32 sums stored to p.part.
+template <class S, bool GLU, bool PARTIAL = false>
 __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs p) {
   __shared__ __attribute__((aligned(1024))) unsigned char a_lds0[S::ATILE];
   __shared__ __attribute__((aligned(1024))) unsigned char b_lds0[S::BTILE];
@@ -128,16 +140,23 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
   __shared__ __attribute__((aligned(1024))) unsigned char b_lds1[S::BTILE];
 
   // ---- which tile ---------------------------------------------------------------
-  const int n_tiles = p.tiles_m * p.tiles_n;
-  const int per_xcd = (n_tiles + kXcds - 1) / kXcds;
-  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-  const int t = xcd * per_xcd + slot;
-  if (t >= n_tiles) return;
-  const int span = kGroupM * p.tiles_n;
-  const int first_m = (t / span) * kGroupM;
-  const int gsize = min(p.tiles_m - first_m, kGroupM);
-  const int tm = first_m + (t % span) % gsize;
-  const int tn = (t % span) / gsize;
+  // whole tiles: the launch's range of the tile order is cut into 8 contiguous
+  // ranges, one per XCD (workgroup i runs on XCD i mod 8); k pieces of tail
+  // tiles: workgroup i runs piece i mod k_parts of tile t_begin + i / k_parts
+  int t, kp = 0;
+  if (PARTIAL) {
+    if ((int)blockIdx.x >= p.t_count * p.k_parts) return;
+    t = p.t_begin + blockIdx.x / p.k_parts;
+    kp = blockIdx.x % p.k_parts;
+  } else {
+    const int count = p.t_count > 0 ? p.t_count : p.tiles_m * p.tiles_n;
+    const int per_xcd = (count + kXcds - 1) / kXcds;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    if (xcd * per_xcd + slot >= count) return;
+    t = p.t_begin + xcd * per_xcd + slot;
+  }
+  int tm, tn;
+  tile_coords(p, t, tm, tn);
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, half = lane >> 5;
   const int wm = wave % S::WAVES_M, wn = wave / S::WAVES_M;
@@ -186,13 +205,14 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
     for (int nb = 0; nb < S::NB; ++nb) acc[mb][nb] = f32x16{};
 
   const int KT = p.K / kTK;
-  copy_tile<S::A_IPW>(Ab, a_rows_bytes, a_lds0, wave * S::A_IPW * 8, va);
-  copy_tile<S::B_IPW>(Wb, b_rows_bytes, b_lds0, wave * S::B_IPW * 8, vb);
-  for (int kt = 0; kt < KT; kt += 2) {
-    k_step<S>(acc, b_rows_bytes, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < KT, wave, va,
+  const int kt0 = PARTIAL ? kp * KT / p.k_parts : 0, kt1 = PARTIAL ? (kp + 1) * KT / p.k_parts : KT;
+  copy_tile<S::A_IPW>(Ab + kt0 * kRowB, a_rows_bytes - kt0 * kRowB, a_lds0, wave * S::A_IPW * 8, va);
+  copy_tile<S::B_IPW>(Wb + kt0 * kRowB, b_rows_bytes - kt0 * kRowB, b_lds0, wave * S::B_IPW * 8, vb);
+  for (int kt = kt0; kt < kt1; kt += 2) {
+    k_step<S>(acc, b_rows_bytes, a_lds0, b_lds0, a_lds1, b_lds1, Ab, Wb, a_rows_bytes, kt, kt + 1 < kt1, wave, va,
               vb, fa, fb);
-    if (kt + 1 < KT)
-      k_step<S>(acc, b_rows_bytes, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < KT, wave,
+    if (kt + 1 < kt1)
+      k_step<S>(acc, b_rows_bytes, a_lds1, b_lds1, a_lds0, b_lds0, Ab, Wb, a_rows_bytes, kt + 1, kt + 2 < kt1, wave,
                 va, vb, fa, fb);
   }
 
@@ -220,7 +240,7 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
   float bias[8];
   {
     bf16x8 bv = bf16x8{};
-    if (!GLU && p.bias) bv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.bias) + n);
+    if (!GLU && !PARTIAL && p.bias) bv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.bias) + n);
 #pragma unroll
     for (int e = 0; e < 8; ++e) bias[e] = (float)bv[e];
   }
@@ -250,6 +270,16 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
       const int64_t m = m0 + wm * S::WM + pass * S::PASS_ROWS + row;
       const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg) ^ (row & 15)) << 4));
       const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + row * 256 + (((2 * cg + 1) ^ (row & 15)) << 4));
+      if (PARTIAL) {
+        // the piece's fp32 sums: [TM][TN] per (tail tile, piece)
+        if (m < p.M) {
+          float *dst = p.part + ((size_t)(t - p.t_begin) * p.k_parts + kp) * (S::TM * S::TN) +
+                       (size_t)(m - m0) * S::TN + (n - n0);
+          *reinterpret_cast<f32x4 *>(dst) = v0;
+          *reinterpret_cast<f32x4 *>(dst + 4) = v1;
+        }
+        continue;
+      }
       if (m < p.M) {
         float o[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         if (GLU) {
@@ -275,6 +305,45 @@ __global__ __launch_bounds__(S::THREADS, 2) void gemm_bf16_kernel(const GemmArgs
   }
 }
 
+// The tail tiles' k pieces summed: C = sum of pieces (+ residual) (+ bias), in
+// the order of the whole-tile epilogue. One thread per 8 columns of a row.
+template <class S>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(const GemmArgs p) {
+  constexpr int CHUNKS = S::TN / 8;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t per_tile = (int64_t)S::TM * CHUNKS;
+  if (gid >= per_tile * p.t_count) return;
+  const int tl = (int)(gid / per_tile);
+  const int row = (int)(gid % per_tile) / CHUNKS, cg = (int)(gid % per_tile) % CHUNKS;
+  int tm, tn;
+  tile_coords(p, p.t_begin + tl, tm, tn);
+  const int64_t m = (int64_t)tm * S::TM + row;
+  if (m >= p.M) return;
+  const int n = tn * S::TN + cg * 8;
+  float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const float *src = p.part + (size_t)tl * p.k_parts * (S::TM * S::TN) + (size_t)row * S::TN + cg * 8;
+  for (int k = 0; k < p.k_parts; ++k) {
+    const f32x4 a = *reinterpret_cast<const f32x4 *>(src + (size_t)k * (S::TM * S::TN));
+    const f32x4 b = *reinterpret_cast<const f32x4 *>(src + (size_t)k * (S::TM * S::TN) + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] += a[e];
+      o[4 + e] += b[e];
+    }
+  }
+  if (p.residual) {
+    const bf16x8 rv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.residual) + m * p.N + n);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] += (float)rv[e];
+  }
+  bf16x8 bv = bf16x8{};
+  if (p.bias) bv = *reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(p.bias) + n);
+  bf16x8 out;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) out[e] = (__bf16)(o[e] + (float)bv[e]);
+  *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(p.C) + m * p.N + n) = out;
+}
+
 using SmallTile = Shape<128, 128, 64, 64>;  // 4 waves, two workgroups per CU
 using LargeTile = Shape<256, 256, 128, 64>;  // 8 waves, one workgroup per CU
 
@@ -290,15 +359,54 @@ hipError_t launch_shape(GemmArgs p, hipStream_t st) {
   return hipGetLastError();
 }
 
-}  // namespace
+// Whole rounds of the resident workgroups as whole tiles, the remaining tiles
+// cut along k into pieces that fill the idle slots, then the reduction.
+template <class S>
+hipError_t launch_split(GemmArgs p, float *part, size_t part_bytes, hipStream_t st) {
+  constexpr int slots = S::THREADS == 256 ? 512 : 256;  // resident workgroups: 2 per CU for 4 waves, else 1
+  p.tiles_m = (int)((p.M + S::TM - 1) / S::TM);
+  p.tiles_n = p.N / S::TN;
+  const int n_tiles = p.tiles_m * p.tiles_n;
+  const int full = n_tiles / slots * slots, tail = n_tiles - full;
+  const int KT = p.K / kTK;
+  const int k_parts = tail > 0 ? std::min(std::min(slots / tail, KT / 4), 8) : 0;
+  if (n_tiles <= 0 || k_parts < 2 || (size_t)tail * k_parts * S::TM * S::TN * 4 > part_bytes)
+    return launch_shape<S>(p, st);
+  if (full > 0) {
+    GemmArgs a = p;
+    a.t_begin = 0;
+    a.t_count = full;
+    gemm_bf16_kernel<S, false><<<dim3(kXcds * ((full + kXcds - 1) / kXcds)), dim3(S::THREADS), 0, st>>>(a);
+  }
+  GemmArgs b = p;
+  b.t_begin = full;
+  b.t_count = tail;
+  b.k_parts = k_parts;
+  b.part = part;
+  gemm_bf16_kernel<S, false, true><<<dim3(tail * k_parts), dim3(S::THREADS), 0, st>>>(b);
+  const int64_t threads = (int64_t)tail * S::TM * (S::TN / 8);
+  gemm_reduce_kernel<S><<<dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st>>>(b);
+  return hipGetLastError();
+}
 
-hipError_t launch_gemm(const GemmArgs &a, hipStream_t st) {
+bool use_large(const GemmArgs &a) {
   // the large tile needs whole output tiles (256 columns, 128 gated) and
   // enough tiles to fill the CUs
   const int out_tn = a.glu ? LargeTile::TN / 2 : LargeTile::TN;
   const int64_t large_tiles = ((a.M + LargeTile::TM - 1) / LargeTile::TM) * (a.N / out_tn);
-  if (a.N % out_tn == 0 && large_tiles >= 2 * 256) return launch_shape<LargeTile>(a, st);
-  return launch_shape<SmallTile>(a, st);
+  return a.N % out_tn == 0 && large_tiles >= 2 * 256;
+}
+
+}  // namespace
+
+hipError_t launch_gemm_split(const GemmArgs &a, float *part, size_t part_bytes, hipStream_t st) {
+  if (a.glu || part == nullptr) return launch_gemm(a, st);
+  return use_large(a) ? launch_split<LargeTile>(a, part, part_bytes, st)
+                      : launch_split<SmallTile>(a, part, part_bytes, st);
+}
+
+hipError_t launch_gemm(const GemmArgs &a, hipStream_t st) {
+  return use_large(a) ? launch_shape<LargeTile>(a, st) : launch_shape<SmallTile>(a, st);
 }
 
 }  // namespace daf

@@ -139,11 +139,13 @@ def _layer_close(got, ref, what):
 
 
 @pytest.mark.parametrize("model,L_d,L_q,n", [(di.TINY_MODEL, 600, 32, 90), (di.TINY_MODEL, 333, 7, 333),
-                                             (di.QWEN7B, 6144, 64, 922)])
+                                             (di.QWEN7B, 6144, 64, 922), (di.QWEN7B, 16384, 128, 2458)])
 def test_decoder_layer_daf(model, L_d, L_q, n):
     """One DAF layer: only the important and question rows are recomputed;
     the hybrid cache receives their roped K/V; the output is the compact
-    state (x of those rows after the layer)."""
+    state (x of those rows after the layer). At the Qwen2.5-7B widths the
+    projections cut their tail tiles along k (986 rows: every tile, in pieces;
+    2586 rows: 512 whole tiles, then 76 in 6 pieces each, then the sum)."""
     import paper_2607_21599_amd as daf
     from oracle import get as oracle_get
     x, kc, vc, idx, wts = _layer_setup(model, L_d, L_q, n, seed=L_d + n)
