@@ -192,6 +192,42 @@ def test_decoder_layer_full():
     _layer_close(_f(xa), ref, "full layer")
 
 
+def test_decoder_layer_full_large_tiles_sampled():
+    """Full recomputation at the Qwen2.5-7B widths with 9300 rows: q_proj,
+    o_proj and the down projection take the 256 x 256 tile (518 tiles: two
+    whole rounds of 256, then 6 tail tiles cut along k, then the sum). The
+    oracle computes K/V for every row and the rest of the layer on sampled
+    rows, including rows of the tail tiles (M-tiles 32-36)."""
+    import paper_2607_21599_amd as daf
+    from oracle import get as oracle_get
+    model, L_d, L_q = di.QWEN7B, 9236, 64
+    x, _, _, _, wts = _layer_setup(model, L_d, L_q, 1, seed=9)
+    T = L_d + L_q
+    cfg = daf.AttnCfg(model.hq, model.hkv, model.d, daf.DAF_BF16)
+    batch = daf.Batch.single(L_d, L_q, 0)
+    w = _weights_on_gpu(model, wts)
+    xa, pos = _dev(x), _dev(np.arange(T, dtype=np.int32))
+    ws_bytes = daf.daf_decoder_layer_workspace_size(cfg, w, batch, daf.DAF_LAYER_FULL)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    daf.daf_decoder_layer(cfg, w, batch, daf.DAF_LAYER_FULL, None, pos, xa, None, None, ws, ws_bytes)
+    torch.cuda.synchronize()
+    rng = np.random.Generator(np.random.PCG64(11))
+    rows = np.union1d(rng.choice(T, 24, replace=False), rng.choice(np.arange(8192, T), 12, replace=False))
+    rows = np.union1d(rows, [0, 255, 256, 8191, 8192, T - 1])
+    f, ow = di.raw_to_f32, _oracle_weights(wts)
+    xf = f(x)
+    h = dec.rmsnorm(xf, ow["w_in"], model.eps)
+    k = dec.rope(dec.linear(h, ow["wk"], ow["bk"]).reshape(T, model.hkv, model.d), np.arange(T), model.theta)
+    v = dec.linear(h, ow["wv"], ow["bv"]).reshape(T, model.hkv, model.d)
+    q = dec.rope(dec.linear(h[rows], ow["wq"], ow["bq"]).reshape(len(rows), model.hq, model.d), rows, model.theta)
+    o = oracle_get().position_attention(q.astype(np.float32), k.astype(np.float32), v.astype(np.float32), rows,
+                                        1.0 / np.sqrt(model.d))[0].reshape(len(rows), -1)
+    x1 = dec.linear(o, ow["wo"], residual=xf[rows])
+    h2 = dec.rmsnorm(x1, ow["w_post"], model.eps)
+    ref = dec.linear(dec.silu_mul(dec.linear(h2, ow["wg"]), dec.linear(h2, ow["wu"])), ow["wd"], residual=x1)
+    _layer_close(_f(xa[torch.from_numpy(rows).cuda()]), ref, "full layer, 256 x 256 tiles, sampled rows")
+
+
 @pytest.mark.parametrize("M,I,K", [(300, 192, 256), (5043, 18944, 3584), (1100, 14848, 512)])
 def test_linear_swiglu(M, I, K):
     """Gate and up projections with SiLU(gate) * up in the epilogue; the last
