@@ -49,7 +49,10 @@
  *   probabilities, so each output row is a weighted mean of value rows with
  *   weights that sum to one; its LSE is the log of that same sum, within
  *   ln(1 + 2^-8) of the exact log-sum-exp (the bf16 rounding of a term that
- *   dominates its row).
+ *   dominates its row). The unnormalised fp32 sums hold probabilities of at most
+ *   2^32 per 16 keys (the running max is raised only past that), so value
+ *   magnitudes times 2^32 per 16 keys must stay within fp32 (|V| below ~1e26
+ *   for 32k keys).
  * Asynchrony. Work is enqueued on `stream` (NULL = the default stream) and the
  *   call returns without synchronising. There is no global state: calls are
  *   re-entrant; calls that write the same buffers must be ordered by the
