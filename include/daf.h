@@ -54,9 +54,10 @@
  *   magnitudes times 2^32 per 16 keys must stay within fp32 (|V| below ~1e26
  *   for 32k keys).
  * Asynchrony. Work is enqueued on `stream` (NULL = the default stream) and the
- *   call returns without synchronising. There is no global state: calls are
- *   re-entrant; calls that write the same buffers must be ordered by the
- *   caller.
+ *   call returns without synchronising. Calls are re-entrant and thread-safe;
+ *   the only state the library keeps is daf_layer_attn's second stream and its
+ *   two events per device (created on first use, guarded by a mutex). Calls
+ *   that write the same buffers must be ordered by the caller.
  * Errors. Every host-visible precondition is checked before anything is
  *   enqueued; on failure the call returns a non-zero daf_status_t, enqueues
  *   nothing, and daf_last_error() describes the problem (thread-local). A
