@@ -58,6 +58,15 @@
  *   the only state the library keeps is daf_layer_attn's second stream and its
  *   two events per device (created on first use, guarded by a mutex). Calls
  *   that write the same buffers must be ordered by the caller.
+ * Graph capture. The calls enqueue kernels and event record/wait operations
+ *   only (no allocation, copy, memset or synchronisation), so a sequence of
+ *   them can be captured into a HIP graph and replayed. daf_layer_attn's
+ *   second stream joins the capture through its fork event and rejoins the
+ *   caller's stream before the call returns. Make the first daf_layer_attn
+ *   call on a device outside any capture (it creates the stream and events),
+ *   and make no daf_layer_attn call on that device from another stream or
+ *   thread while such a capture is open: the shared second stream stays part
+ *   of the capture until it ends.
  * Errors. Every host-visible precondition is checked before anything is
  *   enqueued; on failure the call returns a non-zero daf_status_t, enqueues
  *   nothing, and daf_last_error() describes the problem (thread-local). A
