@@ -14,7 +14,10 @@
 // registers (32 per lane, slab by slab beyond 32k tokens). Scores are
 // non-negative floats, so their bit patterns order like the values: a radix
 // select over 8-bit digits finds the key T of the n-th highest score and how
-// many tokens scoring exactly T to keep. The passes start below the bits that
+// many tokens scoring exactly T to keep. The digit histogram is kept in 32
+// copies, one per lane of a half wave (rows padded to 257 words so that one
+// digit's copies sit in different banks): scores cluster, and with a single
+// copy the lanes of one instruction that share a digit serialise on its word. The passes start below the bits that
 // the lowest and highest key share, so the first histogram spreads over the
 // scores' actual range, and stop early once a digit's keys are all taken.
 // Each wave owns a contiguous range of tokens; a prefix sum over the waves of
@@ -32,6 +35,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kScoreThreads = 256;
 constexpr int kTopnThreads = 1024;
 constexpr int kTopnWaves = kTopnThreads / 64;
+constexpr int kHistCopies = 32, kHistStride = 257;
 
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
@@ -147,7 +151,7 @@ __device__ __forceinline__ unsigned long long ballot(bool x) { return __builtin_
 template <int KPL, bool MULTI>
 __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectLaunch p) {
   constexpr int kSlab = kTopnThreads * KPL, kWaveSlab = kSlab / kTopnWaves;
-  __shared__ int hist[256];
+  __shared__ int hist[kHistCopies * kHistStride];
   __shared__ int wsum[kTopnWaves];
   __shared__ unsigned s_lo[kTopnWaves], s_hi[kTopnWaves], s_prefix;
   __shared__ int s_remaining, s_top;
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectL
     s_lo[wave] = lo;
     s_hi[wave] = hi;
   }
-  if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+  for (int i = threadIdx.x; i < kHistCopies * kHistStride; i += kTopnThreads) hist[i] = 0;
   __syncthreads();
 #pragma unroll
   for (int w = 0; w < kTopnWaves; ++w) {
@@ -216,7 +220,7 @@ __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectL
 #pragma unroll
       for (int j = 0; j < KPL; ++j)
         if (valid(j) && ((k[j] ^ prefix) & decided) == 0u)
-          atomicAdd(&hist[(k[j] >> shift) & ((1u << w) - 1u)], 1);
+          atomicAdd(&hist[(lane & (kHistCopies - 1)) * kHistStride + ((k[j] >> shift) & ((1u << w) - 1u))], 1);
     }
     __syncthreads();
     // digits from the highest down: the selected one holds the remaining-th key
@@ -224,8 +228,11 @@ __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectL
     const int d = (1 << w) - 1 - (int)threadIdx.x;
     int h = 0;
     if (d >= 0) {
-      h = hist[d];
-      hist[d] = 0;  // cleared for the next pass
+#pragma unroll 8
+      for (int c = 0; c < kHistCopies; ++c) {
+        h += hist[c * kHistStride + d];
+        hist[c * kHistStride + d] = 0;  // cleared for the next pass
+      }
     }
     const int above = block_scan(h, wsum);
     if (d >= 0 && above < remaining && above + h >= remaining) {
