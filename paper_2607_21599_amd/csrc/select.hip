@@ -262,16 +262,27 @@ __global__ __launch_bounds__(kTopnThreads) void select_topn_kernel(const SelectL
     const int eq_before = eq_base + wave_scan(n_eq, wsum, eq_total);
     const int eq_keep = max(0, min(n_eq, remaining - eq_before));
     int pos = out_base + wave_scan(n_gt + eq_keep, wsum, kept_total);
-    int eq_seen = 0;
+    if (eq_keep == 0) {
+      // no key equal to T to take in this wave (the usual case): keep the keys above T
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) {
-      const bool v = valid(j);
-      const unsigned long long eq = ballot(v && k[j] == T);
-      const bool keep = (v && k[j] > T) || ((eq >> lane & 1ull) && eq_seen + lanes_below(eq) < eq_keep);
-      const unsigned long long km = ballot(keep);
-      if (keep) out[pos + lanes_below(km)] = slab_base + j * 64 + lane;
-      pos += __popcll(km);
-      eq_seen += __popcll(eq);
+      for (int j = 0; j < KPL; ++j) {
+        const bool keep = valid(j) && k[j] > T;
+        const unsigned long long km = ballot(keep);
+        if (keep) out[pos + lanes_below(km)] = slab_base + j * 64 + lane;
+        pos += __popcll(km);
+      }
+    } else {
+      int eq_seen = 0;
+#pragma unroll
+      for (int j = 0; j < KPL; ++j) {
+        const bool v = valid(j);
+        const unsigned long long eq = ballot(v && k[j] == T);
+        const bool keep = (v && k[j] > T) || ((eq >> lane & 1ull) && eq_seen + lanes_below(eq) < eq_keep);
+        const unsigned long long km = ballot(keep);
+        if (keep) out[pos + lanes_below(km)] = slab_base + j * 64 + lane;
+        pos += __popcll(km);
+        eq_seen += __popcll(eq);
+      }
     }
     out_base += kept_total;
     eq_base += eq_total;
