@@ -89,11 +89,15 @@ daf_status_t parse_batch(const daf_batch_t *b, Batch &out) {
   int64_t tok = 0;
   for (int i = 0; i < b->batch; ++i) {
     Req &q = out.r[i];
-    q.L_d = b->cu_doc[i + 1] - b->cu_doc[i];
-    q.L_q = b->cu_q[i + 1] - b->cu_q[i];
-    q.n = b->cu_imp[i + 1] - b->cu_imp[i];
-    if (q.L_d < 0 || q.L_q < 0 || q.n < 0)
+    // differences in 64 bits: a decreasing pair of int32 entries must not wrap
+    const int64_t L_d = (int64_t)b->cu_doc[i + 1] - b->cu_doc[i];
+    const int64_t L_q = (int64_t)b->cu_q[i + 1] - b->cu_q[i];
+    const int64_t n = (int64_t)b->cu_imp[i + 1] - b->cu_imp[i];
+    if (L_d < 0 || L_q < 0 || n < 0)
       return fail(DAF_ERR_INVALID_ARG, "request %d: prefix arrays must be non-decreasing", i);
+    q.L_d = (int)L_d;  // each lies between 0 and INT32_MAX: the arrays start at 0 and do not decrease
+    q.L_q = (int)L_q;
+    q.n = (int)n;
     if (q.n > q.L_d)
       return fail(DAF_ERR_INVALID_ARG, "request %d: n=%d important tokens exceed L_d=%d", i, q.n, q.L_d);
     q.imp0 = b->cu_imp[i];

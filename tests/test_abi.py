@@ -67,6 +67,10 @@ def test_bad_batches():
         daf.daf_imp_self_attn(c, daf.Batch([0, 10, 5], [0, 1, 2], [0, 1, 2]), FAKE, FAKE, FAKE, FAKE,
                               None, 0)
     assert e.value.status == daf.DAF_ERR_INVALID_ARG
+    with pytest.raises(daf.DafError) as e:  # a decrease whose int32 difference would wrap to positive
+        daf.daf_imp_self_attn(c, daf.Batch([0, 2_000_000_000, -2_000_000_000], [0, 1, 2], [0, 1, 2]), FAKE, FAKE,
+                              FAKE, FAKE, None, 0)
+    assert e.value.status == daf.DAF_ERR_INVALID_ARG
     with pytest.raises(daf.DafError) as e:  # prefix not starting at 0
         daf.daf_imp_self_attn(c, daf.Batch([1, 10], [0, 1], [0, 1]), FAKE, FAKE, FAKE, FAKE, None, 0)
     assert e.value.status == daf.DAF_ERR_INVALID_ARG
