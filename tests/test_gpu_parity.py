@@ -200,8 +200,8 @@ def test_stage2_edge_sizes(L_d, L_q):
     assert_lse_close(_f32(buf["lse_q"]).T, ref["lse_q"], di.BF16, f"stage2 lse {L_d}/{L_q}")
 
 
-@pytest.mark.parametrize("name", ["qwen7b_16k_r05", "qwen7b_16k_r30", "qwen7b_32k", "qwen7b_32k_lq32",
-                                  "qwen7b_128k_r30"])
+@pytest.mark.parametrize("name", ["qwen7b_16k_r05", "qwen7b_16k_r15", "qwen7b_16k_r30", "qwen7b_32k",
+                                  "qwen7b_32k_lq32", "qwen7b_128k_r30"])
 def test_layer_large_sampled(name):
     """Full-size layer through daf_layer_attn, oracle on sampled rows."""
     batch = di.make_batch(di.workload(name))
