@@ -55,7 +55,7 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int kBN = 64;                  // keys per tile
-constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
+[[maybe_unused]] constexpr int kRsrcWord3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
 constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may grow before O is rescaled
 // Full tiles skip the max: a half's probabilities are formed with the running
 // max as it stands, and only if some lane's share of the half's sum exceeds
