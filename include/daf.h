@@ -248,6 +248,27 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
                             void *hidden, void *workspace, size_t ws_bytes,
                             hipStream_t stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, serving
+ * loops or harnesses that forbid hipMalloc): daf_layer_attn with the stage-2
+ * workspace taken from a static device array of the library instead of a
+ * caller buffer, all work on `stream` (no second stream). Arguments and
+ * results as in daf_layer_attn. The array holds daf_layer_noalloc_max_bytes()
+ * bytes (48 MiB) on every device the library runs on, kept until the process
+ * ends; a batch whose workspace (daf_layer_workspace_size) exceeds it returns
+ * DAF_ERR_WORKSPACE and enqueues nothing. The call allocates nothing: no
+ * hipMalloc, hipFree, stream or event creation. Every call on one device
+ * shares that device's array, so calls that can overlap on one device (other
+ * streams, other threads) race; order them on one stream. No result depends on
+ * what an earlier call left in the array. */
+size_t daf_layer_noalloc_max_bytes(void);
+daf_status_t daf_layer_attn_noalloc(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
+                                    const int32_t *idx, const void *q_imp,
+                                    const void *k_imp, const void *v_imp,
+                                    const void *q_q, const void *k_q, const void *v_q,
+                                    void *k_cache, void *v_cache, void *o_imp,
+                                    float *lse_imp, void *o_q, float *lse_q,
+                                    void *hidden, hipStream_t stream);
+
 /* Debug check of the index precondition: writes to *d_bad_count (device
  * int32) the number of entries of idx that are out of [0, L_d,b) or not
  * greater than their predecessor in the same request. */

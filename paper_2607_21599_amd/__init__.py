@@ -17,7 +17,8 @@ __all__ = [
     "DAF_OK", "DAF_BF16", "DAF_F32", "DAF_SRC_TOKENS", "DAF_SRC_DOCS", "DAF_FUSE_KV",
     "DAF_FUSE_HIDDEN", "DafError", "AttnCfg", "Batch", "lib", "library_path",
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
-    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
+    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_layer_noalloc_max_bytes",
+    "daf_layer_attn_noalloc", "daf_check_indices", "daf_select_important",
     "daf_linear", "daf_linear_swiglu", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
     "daf_decoder_layer", "LayerWeights", "DAF_LAYER_DAF", "DAF_LAYER_FULL",
     "daf_status_string", "daf_last_error", "daf_version", "EXPORTED",
@@ -33,7 +34,8 @@ DAF_LAYER_DAF, DAF_LAYER_FULL = 0, 1
 # every symbol include/daf.h declares
 EXPORTED = [
     "daf_gather_important", "daf_imp_self_attn", "daf_position_attn", "daf_qdoc_workspace_size", "daf_qdoc_attn",
-    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_check_indices", "daf_select_important",
+    "daf_fuse", "daf_layer_workspace_size", "daf_layer_attn", "daf_layer_noalloc_max_bytes",
+    "daf_layer_attn_noalloc", "daf_check_indices", "daf_select_important",
     "daf_linear", "daf_linear_swiglu", "daf_rmsnorm", "daf_rope", "daf_silu_mul", "daf_decoder_layer_workspace_size",
     "daf_decoder_layer", "daf_status_string", "daf_last_error", "daf_version",
 ]
@@ -121,6 +123,8 @@ def lib() -> ctypes.CDLL:
             "daf_fuse": (i32, [cfgp, bp, u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
             "daf_layer_workspace_size": (sz, [cfgp, bp]),
             "daf_layer_attn": (i32, [cfgp, bp, _vp] + [_vp] * 13 + [_vp, sz, _vp]),
+            "daf_layer_noalloc_max_bytes": (sz, []),
+            "daf_layer_attn_noalloc": (i32, [cfgp, bp, _vp] + [_vp] * 13 + [_vp]),
             "daf_check_indices": (i32, [bp, _vp, _vp, _vp]),
             "daf_linear": (i32, [i64, i32, i32, _vp, _vp, _vp, _vp, _vp, _vp]),
             "daf_linear_swiglu": (i32, [i64, i32, i32, _vp, _vp, _vp, _vp]),
@@ -266,6 +270,18 @@ def daf_layer_attn(cfg: AttnCfg, batch: Batch, idx, q_imp, k_imp, v_imp, q_q, k_
                                 _ptr(v_imp), _ptr(q_q), _ptr(k_q), _ptr(v_q), _ptr(k_cache),
                                 _ptr(v_cache), _ptr(o_imp), _ptr(lse_imp), _ptr(o_q), _ptr(lse_q),
                                 _ptr(hidden), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def daf_layer_noalloc_max_bytes() -> int:
+    return int(lib().daf_layer_noalloc_max_bytes())
+
+
+def daf_layer_attn_noalloc(cfg: AttnCfg, batch: Batch, idx, q_imp, k_imp, v_imp, q_q, k_q, v_q, k_cache,
+                           v_cache, o_imp, lse_imp, o_q, lse_q, hidden, stream=None):
+    _check(lib().daf_layer_attn_noalloc(_cfgp(cfg), _bp(batch), _ptr(idx), _ptr(q_imp), _ptr(k_imp),
+                                        _ptr(v_imp), _ptr(q_q), _ptr(k_q), _ptr(v_q), _ptr(k_cache),
+                                        _ptr(v_cache), _ptr(o_imp), _ptr(lse_imp), _ptr(o_q), _ptr(lse_q),
+                                        _ptr(hidden), _stream(stream)))
 
 
 def daf_check_indices(batch: Batch, idx, d_bad_count, stream=None):

@@ -225,6 +225,44 @@ AuxStream *aux_stream() {
   return a.ok ? &a : nullptr;
 }
 
+// ---- static scratch for the allocation-free layer call ------------------------
+// daf_layer_attn_noalloc takes its stage-2 workspace from this array instead of
+// a caller buffer. In host code `scratch` names a host-side stand-in, never the
+// device memory: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and only that address is
+// passed to kernels.
+constexpr size_t kScratchBytes = (size_t)48 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchAddr {
+  void *ptr = nullptr;
+  bool tried = false;
+  hipError_t err = hipSuccess;
+};
+std::mutex g_scratch_mu;
+ScratchAddr g_scratch[kMaxDevices];
+
+// the current device's scratch address, or null with `err` set
+void *scratch_ptr(hipError_t &err) {
+  int dev = -1;
+  err = hipGetDevice(&dev);
+  if (err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) {
+    err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ScratchAddr &a = g_scratch[dev];
+  if (!a.tried) {
+    a.tried = true;
+    void *p = nullptr;
+    a.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (a.err == hipSuccess) a.ptr = p;
+  }
+  err = a.err;
+  return a.ptr;
+}
+
 // ---- attention work tables ----------------------------------------------------
 AttnEntry self_entry(const Cfg &c, const Req &q, int64_t total_imp, const void *q_imp,
                      const void *k_imp, const void *v_imp, void *o_imp, float *lse_imp) {
@@ -454,7 +492,8 @@ daf_status_t check_fuse_ptrs(const Batch &b, uint32_t flags, const int32_t *idx,
 daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, const void *q_imp,
                              const void *k_imp, const void *v_imp, const void *q_q, const void *k_q,
                              const void *v_q, void *k_cache, void *v_cache, void *o_imp, float *lse_imp, void *o_q,
-                             float *lse_q, void *hidden, void *workspace, size_t ws_bytes, hipStream_t stream) {
+                             float *lse_q, void *hidden, void *workspace, size_t ws_bytes, hipStream_t stream,
+                             bool fork = true) {
   // plan (and check the workspace) before enqueueing anything
   std::vector<AttnEntry> self, qdoc;
   std::vector<MergeEntry> merge;
@@ -468,7 +507,7 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
   // and the merge (question rows of hidden) touch none of that, so stage 1
   // runs beside them on the second stream.
   std::lock_guard<std::mutex> lock(g_aux_mu);
-  AuxStream *ax = self.empty() ? nullptr : aux_stream();
+  AuxStream *ax = (self.empty() || !fork) ? nullptr : aux_stream();
   daf_status_t st1 = DAF_OK;
   daf_status_t st = fuse_impl(c, b, DAF_FUSE_KV, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, nullptr,
                               nullptr, nullptr, stream);
@@ -1016,6 +1055,40 @@ daf_status_t daf_layer_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,
     if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
     return layer_attn_impl(c, b, idx, q_imp, k_imp, v_imp, q_q, k_q, v_q, k_cache, v_cache, o_imp, lse_imp, o_q,
                            lse_q, hidden, workspace, ws_bytes, stream);
+  } catch (...) {
+    return fail(DAF_ERR_HIP, "unexpected host exception");
+  }
+}
+
+size_t daf_layer_noalloc_max_bytes(void) { return kScratchBytes; }
+
+daf_status_t daf_layer_attn_noalloc(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, const int32_t *idx,
+                                    const void *q_imp, const void *k_imp, const void *v_imp, const void *q_q,
+                                    const void *k_q, const void *v_q, void *k_cache, void *v_cache, void *o_imp,
+                                    float *lse_imp, void *o_q, float *lse_q, void *hidden, hipStream_t stream) {
+  try {
+    Cfg c;
+    Batch b;
+    CHECK(parse_cfg(cfg, c));
+    CHECK(parse_batch(batch, b));
+    CHECK(check_kv_extent(c, b));
+    const uint32_t both = DAF_FUSE_KV | DAF_FUSE_HIDDEN;
+    if (b.total_imp == 0 && b.total_q == 0) return ok();
+    CHECK(check_fuse_ptrs(b, both, idx, k_imp, v_imp, k_q, v_q, k_cache, v_cache, o_imp, o_q, hidden));
+    if (b.total_imp > 0) CHECK(need_ptr(q_imp, "q_imp"));
+    if (b.total_q > 0) CHECK(need_ptr(q_q, "q_q"));
+    if (lse_imp) CHECK(need_ptr(lse_imp, "lse_imp"));
+    if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
+    const size_t need = ws_layout(c, b, plan_splits(c, b)).total;
+    if (need > kScratchBytes)
+      return fail(DAF_ERR_WORKSPACE, "this batch needs %zu bytes of scratch; the allocation-free call has %zu",
+                  need, kScratchBytes);
+    hipError_t e = hipSuccess;
+    void *ws = scratch_ptr(e);
+    if (!ws) return hip_fail(e, "scratch address lookup");
+    // one stream: the second stream of daf_layer_attn is created on first use
+    return layer_attn_impl(c, b, idx, q_imp, k_imp, v_imp, q_q, k_q, v_q, k_cache, v_cache, o_imp, lse_imp, o_q,
+                           lse_q, hidden, ws, kScratchBytes, stream, false);
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");
   }
