@@ -52,7 +52,9 @@
  *   dominates its row). The unnormalised fp32 sums hold probabilities of at most
  *   2^32 per 16 keys (the running max is raised only past that), so value
  *   magnitudes times 2^32 per 16 keys must stay within fp32 (|V| below ~1e26
- *   for 32k keys).
+ *   for 32k keys). Stage 2's key splits keep their normalised partial outputs
+ *   in the input dtype (bf16: one more rounding of each split's weighted mean
+ *   before the log-sum-exp merge) and their LSE in fp32.
  * Asynchrony. Work is enqueued on `stream` (NULL = the default stream) and the
  *   call returns without synchronising. Calls are re-entrant and thread-safe;
  *   the only state the library keeps is daf_layer_attn's second stream and its
@@ -200,7 +202,8 @@ size_t daf_qdoc_workspace_size(const daf_attn_cfg_t *cfg,
  *   (the hybrid cache: daf_fuse(DAF_FUSE_KV) first) -> o_q [sum L_q][Hq][D];
  *   lse_q: nullable float32 [Hq][sum L_q].
  * Question row j of request b attends cache rows 0 .. L_d,b + j. The keys are
- * split across workgroups; partial results live in `workspace` (at least
+ * split across workgroups; partial results (each split's normalised output in
+ * the input dtype and its fp32 LSE) live in `workspace` (at least
  * daf_qdoc_workspace_size bytes, 16-byte aligned, contents undefined after
  * the call) and are merged by log-sum-exp. */
 daf_status_t daf_qdoc_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch,

@@ -189,7 +189,9 @@ WsLayout ws_layout(const Cfg &c, const Batch &b, const std::vector<Split> &sp) {
   WsLayout w{};
   w.part_rows = 0;
   for (size_t i = 0; i < b.r.size(); ++i) w.part_rows += (int64_t)b.r[i].L_q * sp[i].n_splits;
-  w.part_o_bytes = align_up((size_t)w.part_rows * c.hq * c.d * sizeof(float));
+  // partial outputs in the input dtype (normalised, so bf16 keeps their precision
+  // relative to the values), their LSE in fp32
+  w.part_o_bytes = align_up((size_t)w.part_rows * c.hq * c.d * c.elem);
   w.part_lse_bytes = align_up((size_t)w.part_rows * c.hq * sizeof(float));
   w.total = w.part_o_bytes + w.part_lse_bytes;
   return w;
@@ -285,7 +287,7 @@ AttnEntry self_entry(const Cfg &c, const Req &q, int64_t total_imp, const void *
 }
 
 AttnEntry qdoc_entry(const Cfg &c, const Req &q, const Split &sp, int64_t part_row0,
-                     const void *q_q, const void *k_cache, const void *v_cache, float *part_o,
+                     const void *q_q, const void *k_cache, const void *v_cache, char *part_o,
                      float *part_lse) {
   AttnEntry e{};
   const size_t qrow = (size_t)c.hq * c.d * c.elem, krow = (size_t)c.hkv * c.d * c.elem;
@@ -294,7 +296,7 @@ AttnEntry qdoc_entry(const Cfg &c, const Req &q, const Split &sp, int64_t part_r
   e.v = static_cast<const char *>(v_cache) + q.tok0 * krow;
   e.o = nullptr;
   e.lse = nullptr;
-  e.part_o = part_o + part_row0 * c.hq * c.d;
+  e.part_o = part_o + part_row0 * c.hq * c.d * c.elem;
   e.part_lse = part_lse + part_row0 * c.hq;
   e.n_rows = q.L_q;
   e.n_keys = q.L_d + q.L_q;
@@ -361,7 +363,7 @@ daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const v
   if (ws_bytes < w.total) return fail(DAF_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, w.total);
   if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
     return fail(DAF_ERR_ALIGNMENT, "workspace is not 16-byte aligned");
-  float *part_o = static_cast<float *>(workspace);
+  char *part_o = static_cast<char *>(workspace);
   float *part_lse = reinterpret_cast<float *>(static_cast<char *>(workspace) + w.part_o_bytes);
   int64_t prow = 0;
   const size_t qrow = (size_t)c.hq * c.d * c.elem;
@@ -370,7 +372,7 @@ daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const v
     if (q.L_q == 0) continue;
     out.push_back(qdoc_entry(c, q, sp[i], prow, q_q, k_cache, v_cache, part_o, part_lse));
     MergeEntry m{};
-    m.part_o = part_o + prow * c.hq * c.d;
+    m.part_o = part_o + prow * c.hq * c.d * c.elem;
     m.part_lse = part_lse + prow * c.hq;
     m.o = static_cast<char *>(o_q) + q.q0 * qrow;
     m.lse = lse_q ? lse_q + q.q0 : nullptr;

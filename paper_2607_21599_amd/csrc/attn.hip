@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(const AttnLau
     if (E.lse != nullptr && half == 0) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
   } else {
     const size_t prow = (size_t)my_row * E.n_splits + s;
-    float *op = E.part_o + (prow * p.hq + h) * D + 4 * half;
+    float *op = static_cast<float *>(E.part_o) + (prow * p.hq + h) * D + 4 * half;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -344,7 +344,8 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
   const int sb = hs * per_half, se = min(S, sb + per_half);
   const size_t prow0 = (size_t)r * S;
   const float *lse = E.part_lse + prow0 * p.hq + h;
-  const float *src = E.part_o + (prow0 * p.hq + h) * D + 4 * t;
+  // partial outputs in the output dtype T: 4 features (8 or 16 bytes) per thread and split
+  const T *src = static_cast<const T *>(E.part_o) + (prow0 * p.hq + h) * D + 4 * t;
   const size_t split_stride = (size_t)p.hq * D;
   constexpr int U = 16;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -356,7 +357,9 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(const MergeLaunch p) {
     for (int u = 0; u < U; ++u) {
       if (s0 + u < se) {
         ls[u] = lse[(size_t)(s0 + u) * p.hq];
-        po[u] = *reinterpret_cast<const f32x4 *>(src + (s0 + u) * split_stride);
+        const typename Vec<T>::v4 v = *reinterpret_cast<const typename Vec<T>::v4 *>(src + (s0 + u) * split_stride);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) po[u][j] = (float)v[j];
       } else {
         ls[u] = -INFINITY;
         po[u] = f32x4{0.f, 0.f, 0.f, 0.f};

@@ -504,23 +504,20 @@ __device__ __forceinline__ void attn_job(const AttnLaunch &p, const int xcd, con
       });
     if (E.lse != nullptr && half == 0 && my_row < n_rows) E.lse[(size_t)h * E.lse_stride + my_row] = lse_nat;
   } else {
-    // fp32 partials: two passes over half the features each (ROWB bytes per row)
+    // bf16 partials (the normalised split output, like a final output row)
 #pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int db2 = 0; db2 < DB / 2; ++db2)
+      for (int q4 = 0; q4 < 4; ++q4) {
+        bf16x4 v;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          f32x4 v;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) v[t] = w.oacc[pass * (DB / 2) + db2][4 * q4 + t] * inv;
-          stage_put<D>(stg, l32, 8 * db2 + 2 * q4 + half, 0, v);
-        }
-      store_rows<D>(stg, lane, wrow, n_rows, [&](int r) {
-        const size_t prow = (size_t)r * E.n_splits + s;
-        return reinterpret_cast<unsigned char *>(E.part_o + (prow * p.hq + h) * D) + pass * Gm::ROWB;
-      });
-    }
+        for (int t = 0; t < 4; ++t) v[t] = (__bf16)(w.oacc[db][4 * q4 + t] * inv);
+        stage_put<D>(stg, l32, 4 * db + q4, 8 * half, v);
+      }
+    store_rows<D>(stg, lane, wrow, n_rows, [&](int r) {
+      const size_t prow = (size_t)r * E.n_splits + s;
+      return static_cast<unsigned char *>(E.part_o) + (prow * p.hq + h) * D * 2;
+    });
     if (half == 0 && my_row < n_rows) E.part_lse[((size_t)my_row * E.n_splits + s) * p.hq + h] = lse_nat;
   }
 }

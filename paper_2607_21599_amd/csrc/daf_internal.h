@@ -27,7 +27,8 @@ struct AttnEntry {
   const void *v;
   void *o;         // [n_rows][Hq][D] final output (direct mode), else null
   float *lse;      // [Hq][lse_stride] at this request's first column, nullable
-  float *part_o;   // split mode: [n_rows * n_splits][Hq][D] fp32
+  void *part_o;    // split mode: [n_rows * n_splits][Hq][D], normalised partial outputs in the input
+                   // dtype (bf16 or fp32)
   float *part_lse; // split mode: [n_rows * n_splits][Hq]
   int32_t lse_stride;
   int32_t n_rows;
@@ -75,7 +76,7 @@ struct AttnLaunch {
 
 // Log-sum-exp merge of split partials, one request per entry.
 struct MergeEntry {
-  const float *part_o;
+  const void *part_o;  // [rows * n_splits][Hq][D] in the input dtype
   const float *part_lse;
   void *o;        // [n_rows][Hq][D]
   float *lse;     // nullable, [Hq][lse_stride] at the request's first column
