@@ -104,8 +104,9 @@ def test_workspace_checks():
     b = daf.Batch.single(32768, 128, 4915)
     need = daf.daf_qdoc_workspace_size(c, b)
     assert need == daf.daf_layer_workspace_size(c, b)
-    # 128 rows x 18 splits x 28 heads x (128 + 1) fp32, each region 256-byte aligned
-    assert need == 128 * 18 * 28 * 128 * 4 + ((128 * 18 * 28 * 4 + 255) // 256) * 256
+    # 128 rows x 18 splits x 28 heads: 128 bf16 partial outputs and one fp32 LSE,
+    # each region 256-byte aligned
+    assert need == 128 * 18 * 28 * 128 * 2 + ((128 * 18 * 28 * 4 + 255) // 256) * 256
     for ws, nbytes, status in [(None, need, daf.DAF_ERR_WORKSPACE), (FAKE, need - 1, daf.DAF_ERR_WORKSPACE),
                                (FAKE + 4, need, daf.DAF_ERR_ALIGNMENT)]:
         with pytest.raises(daf.DafError) as e:
