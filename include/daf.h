@@ -5,9 +5,9 @@
  * DAF (Sec. 2 of the paper) replaces full prefill attention over retrieved
  * documents whose KV caches were computed offline, one document at a time, by
  * three stages per layer:
- *   1. important-token self-attention: the n = r*L_d important tokens are
- *      gathered from all documents into a condensed sequence and attend only to
- *      each other (Sec. 2 item 1; Complexity Analysis);
+ *   1. important-token self-attention: n = r*L_d selected rows, taken from
+ *      every document, form one packed array whose queries see only keys of
+ *      that array (Sec. 2 item 1; Complexity Analysis);
  *   2. question-document attention: the L_q question tokens, at the tail of the
  *      sequence, attend over all L_d + L_q keys, reading a hybrid KV cache in
  *      which the important tokens' rows already hold their recomputed K/V
@@ -128,9 +128,8 @@ enum {
   DAF_FUSE_HIDDEN = 2 /* stage outputs into the hidden states */
 };
 
-/* Gather the important rows into a condensed sequence (Sec. 2 item 1: the
- * important tokens of all documents are gathered into one condensed
- * sequence).
+/* Gather the important rows into one contiguous array per batch (the row
+ * collection step of stage 1, Sec. 2 item 1).
  *   dst[cu_imp[b] + i] = src[base_b + idx[cu_imp[b] + i]]   (row_bytes each)
  * with base_b = tok_b for DAF_SRC_TOKENS or cu_doc[b] for DAF_SRC_DOCS. Rows
  * are copied bit for bit; row_bytes must be a positive multiple of 16. Used

@@ -12,10 +12,10 @@
  * representable in double, so the oracle's own error is rounding of fp64 sums.
  *
  * Paper sections followed:
- *   - Sec. 2 item 1 (important-token selection & self-attention): gathering the
- *     important tokens from all documents into a condensed sequence and
- *     attending only among them; the Complexity Analysis paragraph fixes that
- *     the important tokens attend only to each other.
+ *   - Sec. 2 item 1 (important-token selection & self-attention): the selected
+ *     rows of every document are packed into one array, and each of them
+ *     attends over keys from that array alone (the Complexity Analysis
+ *     paragraph gives the same key set).
  *   - Sec. 2 item 2 (question-document self-attention): question rows attend
  *     over an L_q x (L_d + L_q) matrix whose keys are all preceding document
  *     tokens and the question itself, using the hybrid KV cache in which the
@@ -49,8 +49,8 @@ int daf_oracle_mutant(void) { return DAF_ORACLE_MUTANT; }
 /* Threads the OpenMP loops of this library use. */
 int daf_oracle_threads(void) { return omp_get_max_threads(); }
 
-/* Row gather, byte for byte: dst[i] = src[rows[i]].  (Sec. 2 item 1: the
- * important tokens are gathered into a condensed sequence.) */
+/* Row gather, byte for byte: dst[i] = src[rows[i]]  (the row collection of
+ * Sec. 2 item 1). */
 void daf_oracle_gather_rows(const uint8_t *src, int64_t row_bytes,
                             const int64_t *rows, int64_t nrows, uint8_t *dst) {
   int64_t count = nrows;

@@ -352,9 +352,15 @@ void add_self_entries(const Cfg &c, const Batch &b, const void *q_imp, const voi
   }
 }
 
+// Stage-2 work of one call: the attention work table and the merge of the
+// split partials.
+struct QdocPlan {
+  std::vector<AttnEntry> attn;
+  std::vector<MergeEntry> merge;
+};
+
 daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const void *k_cache,
-                          const void *v_cache, void *workspace, size_t ws_bytes,
-                          std::vector<AttnEntry> &out, std::vector<MergeEntry> &merge, void *o_q,
+                          const void *v_cache, void *workspace, size_t ws_bytes, QdocPlan &plan, void *o_q,
                           float *lse_q, void *hidden = nullptr) {
   const std::vector<Split> sp = plan_splits(c, b);
   const WsLayout w = ws_layout(c, b, sp);
@@ -370,7 +376,7 @@ daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const v
   for (size_t i = 0; i < b.r.size(); ++i) {
     const Req &q = b.r[i];
     if (q.L_q == 0) continue;
-    out.push_back(qdoc_entry(c, q, sp[i], prow, q_q, k_cache, v_cache, part_o, part_lse));
+    plan.attn.push_back(qdoc_entry(c, q, sp[i], prow, q_q, k_cache, v_cache, part_o, part_lse));
     MergeEntry m{};
     m.part_o = part_o + prow * c.hq * c.d * c.elem;
     m.part_lse = part_lse + prow * c.hq;
@@ -383,7 +389,7 @@ daf_status_t qdoc_entries(const Cfg &c, const Batch &b, const void *q_q, const v
       m.o2 = hidden;
       m.o2_row0 = q.tok0 + q.L_d;
     }
-    merge.push_back(m);
+    plan.merge.push_back(m);
     prow += (int64_t)q.L_q * sp[i].n_splits;
   }
   return DAF_OK;
@@ -402,10 +408,16 @@ daf_status_t run_merge(const Cfg &c, std::vector<MergeEntry> &merge, hipStream_t
       p.e[p.n_entries++] = m;
     }
     p.total_rows = rows;
-    hipError_t err = launch_merge(c.dtype, c.d, p, st);
+    hipError_t err = c.dtype == DAF_BF16 ? launch_qdoc_merge_bf16(c.d, p, st) : launch_merge(c.dtype, c.d, p, st);
     if (err != hipSuccess) return hip_fail(err, "merge launch");
   }
   return DAF_OK;
+}
+
+// Stage 2 and its merge.
+daf_status_t run_qdoc(const Cfg &c, QdocPlan &plan, hipStream_t st) {
+  CHECK(run_entries(c, AttnKind::kQdoc, plan.attn, st));
+  return run_merge(c, plan.merge, st);
 }
 
 // ---- row movement ---------------------------------------------------------------
@@ -497,13 +509,13 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
                              float *lse_q, void *hidden, void *workspace, size_t ws_bytes, hipStream_t stream,
                              bool fork = true) {
   // plan (and check the workspace) before enqueueing anything
-  std::vector<AttnEntry> self, qdoc;
-  std::vector<MergeEntry> merge;
+  std::vector<AttnEntry> self;
+  QdocPlan qdoc;
   // the epilogues also fuse the outputs into the hidden states: stage-1 row i
   // of request b goes to hidden[tok_b + idx[i]], question row j (written by
   // the merge) to hidden[tok_b + L_d,b + j]
   add_self_entries(c, b, q_imp, k_imp, v_imp, o_imp, lse_imp, self, hidden, idx);
-  CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, merge, o_q, lse_q, hidden));
+  CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, qdoc, o_q, lse_q, hidden));
   // Stage 1 reads only the condensed q/k/v and writes o_imp and the
   // important rows of hidden; the hybrid KV (which stage 2 reads), stage 2
   // and the merge (question rows of hidden) touch none of that, so stage 1
@@ -517,8 +529,7 @@ daf_status_t layer_attn_impl(const Cfg &c, const Batch &b, const int32_t *idx, c
   // enqueued before stage 1, so stage 2's workgroups are dispatched first and
   // stage 1 fills in behind them (measured 1-2% faster than stage 1 first)
   hipError_t ef = ax ? hipEventRecord(ax->fork, stream) : hipSuccess;
-  if (st == DAF_OK) st = run_entries(c, AttnKind::kQdoc, qdoc, stream);
-  if (st == DAF_OK) st = run_merge(c, merge, stream);
+  if (st == DAF_OK) st = run_qdoc(c, qdoc, stream);
   if (ax) {
     if (ef == hipSuccess) ef = hipStreamWaitEvent(ax->s, ax->fork, 0);
     if (ef != hipSuccess) return hip_fail(ef, "stream fork");
@@ -1009,11 +1020,9 @@ daf_status_t daf_qdoc_attn(const daf_attn_cfg_t *cfg, const daf_batch_t *batch, 
     CHECK(need_ptr(v_cache, "v_cache"));
     CHECK(need_ptr(o_q, "o_q"));
     if (lse_q) CHECK(need_ptr(lse_q, "lse_q"));
-    std::vector<AttnEntry> entries;
-    std::vector<MergeEntry> merge;
-    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, entries, merge, o_q, lse_q));
-    CHECK(run_entries(c, AttnKind::kQdoc, entries, stream));
-    CHECK(run_merge(c, merge, stream));
+    QdocPlan plan;
+    CHECK(qdoc_entries(c, b, q_q, k_cache, v_cache, workspace, ws_bytes, plan, o_q, lse_q));
+    CHECK(run_qdoc(c, plan, stream));
     return ok();
   } catch (...) {
     return fail(DAF_ERR_HIP, "unexpected host exception");

@@ -580,11 +580,101 @@ hipError_t launch_t(AttnKind kind, const AttnLaunch &p0, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ---- merge of the stage-2 split partials ---------------------------------------
+//
+// Merge of the bf16 split partials: one wave per (question row, query head).
+// Lane = split group * CHN + chunk: each lane accumulates one 8-feature chunk
+// over every SG-th split (online log-sum-exp), then the split groups combine
+// across lanes.
+template <int D>
+__global__ __launch_bounds__(256) void qdoc_merge_kernel(const MergeLaunch p) {
+  constexpr int CHN = D / 8, SG = 64 / CHN;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, c = lane % CHN, sg = lane / CHN;
+  const int row = item / p.hq, h = item % p.hq;
+  if (row >= p.total_rows) return;  // whole waves leave together
+  int ei = 0;
+  while (ei + 1 < p.n_entries && p.e[ei + 1].row0 <= row) ++ei;
+  const MergeEntry &E = p.e[ei];
+  const int r = row - E.row0;
+  const int S = E.n_splits;
+  const size_t prow0 = (size_t)r * S;
+  const float *lse = E.part_lse + prow0 * p.hq + h;
+  const __bf16 *src = static_cast<const __bf16 *>(E.part_o) + (prow0 * p.hq + h) * D + 8 * c;
+  const size_t sstride = (size_t)p.hq * D;
+  constexpr int U = 8;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, wsum = 0.f;
+  for (int s0 = sg; s0 < S; s0 += SG * U) {
+    float ls[U];
+    bf16x8 po[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int sx = s0 + u * SG;
+      if (sx < S) {
+        ls[u] = lse[(size_t)sx * p.hq];
+        po[u] = *reinterpret_cast<const bf16x8 *>(src + sx * sstride);
+      } else {
+        ls[u] = -INFINITY;
+        po[u] = bf16x8{};
+      }
+    }
+    float mc = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u) mc = fmaxf(mc, ls[u]);
+    const float a = (m == -INFINITY) ? 0.f : __expf(m - mc);
+    wsum *= a;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] *= a;
+    m = mc;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float wt = (ls[u] == -INFINITY) ? 0.f : __expf(ls[u] - m);
+      wsum += wt;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] += wt * (float)po[u][k];
+    }
+  }
+  // combine the SG split groups (lanes c, c + CHN, c + 2 CHN, ...)
+#pragma unroll
+  for (int off = CHN; off < 64; off *= 2) {
+    const float m2 = __shfl_xor(m, off, 64), w2 = __shfl_xor(wsum, off, 64);
+    const float mm = fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : __expf(m - mm);
+    const float b = (m2 == -INFINITY) ? 0.f : __expf(m2 - mm);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = acc[k] * a + __shfl_xor(acc[k], off, 64) * b;
+    wsum = wsum * a + w2 * b;
+    m = mm;
+  }
+  if (sg != 0) return;
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  bf16x8 out;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) out[k] = (__bf16)(acc[k] * inv);
+  *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(E.o) + ((size_t)r * p.hq + h) * D + 8 * c) = out;
+  if (E.o2 != nullptr)
+    *reinterpret_cast<bf16x8 *>(static_cast<__bf16 *>(E.o2) + ((size_t)(E.o2_row0 + r) * p.hq + h) * D + 8 * c) = out;
+  if (E.lse != nullptr && c == 0) E.lse[(size_t)h * E.lse_stride + r] = wsum > 0.f ? m + __logf(wsum) : -INFINITY;
+}
+
+template <int D>
+hipError_t launch_qdoc_merge_t(const MergeLaunch &p, hipStream_t st) {
+  const int64_t items = (int64_t)p.total_rows * p.hq;
+  qdoc_merge_kernel<D><<<dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st>>>(p);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_attention_bf16(int head_dim, AttnKind kind, const AttnLaunch &p, hipStream_t st) {
   if (p.n_groups <= 0) return hipSuccess;
   return head_dim == 128 ? launch_t<128>(kind, p, st) : launch_t<64>(kind, p, st);
+}
+
+hipError_t launch_qdoc_merge_bf16(int head_dim, const MergeLaunch &p, hipStream_t st) {
+  if (p.total_rows <= 0) return hipSuccess;
+  return head_dim == 128 ? launch_qdoc_merge_t<128>(p, st) : launch_qdoc_merge_t<64>(p, st);
 }
 
 }  // namespace daf

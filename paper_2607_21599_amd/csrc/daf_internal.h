@@ -152,6 +152,8 @@ hipError_t launch_attention_bf16(int head_dim, AttnKind kind, const AttnLaunch &
                                  hipStream_t s);
 hipError_t launch_merge(int dtype, int head_dim, const MergeLaunch &p,
                         hipStream_t s);
+// merge of the bf16 stage-2 split partials (attn_bf16.hip)
+hipError_t launch_qdoc_merge_bf16(int head_dim, const MergeLaunch &p, hipStream_t s);
 hipError_t launch_gather(const RowLaunch &p, int64_t src_base_unused,
                          const void *src, void *dst, hipStream_t s);
 hipError_t launch_scatter(const RowLaunch &p, const ScatterPair *pairs,

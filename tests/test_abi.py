@@ -107,6 +107,11 @@ def test_workspace_checks():
     # 128 rows x 18 splits x 28 heads: 128 bf16 partial outputs and one fp32 LSE,
     # each region 256-byte aligned
     assert need == 128 * 18 * 28 * 128 * 2 + ((128 * 18 * 28 * 4 + 255) // 256) * 256
+    # a 32-row question: 7 (head, 32-row) units per KV head in 2 workgroups,
+    # 8 workgroups per split over 513 key tiles; about 512 workgroups of equal
+    # share give splits of 9 tiles, so 57 splits
+    b32 = daf.Batch.single(32768, 32, 4915)
+    assert daf.daf_qdoc_workspace_size(c, b32) == 32 * 57 * 28 * 128 * 2 + ((32 * 57 * 28 * 4 + 255) // 256) * 256
     for ws, nbytes, status in [(None, need, daf.DAF_ERR_WORKSPACE), (FAKE, need - 1, daf.DAF_ERR_WORKSPACE),
                                (FAKE + 4, need, daf.DAF_ERR_ALIGNMENT)]:
         with pytest.raises(daf.DafError) as e:

@@ -65,13 +65,13 @@ def test_noalloc_two_calls_second_smaller():
 
 
 def test_noalloc_refuses_oversized_batch():
-    """A question of 4096 rows needs more stage-2 workspace than the static
-    array holds: the call returns DAF_ERR_WORKSPACE and writes nothing. Every
+    """A question of 8192 rows needs more stage-2 workspace than the static
+    array holds (one key split: 8192 x 28 bf16 partial rows, 58.7 MB): the call returns DAF_ERR_WORKSPACE and writes nothing. Every
     buffer is real and sized for the shape, so even a launch would stay in
     bounds."""
     import paper_2607_21599_amd as daf
     from paper_2607_21599_amd.tensors import LayerBuffers
-    shape = di.Shape("big_q", L_d=1000, L_q=4096, n=100, hq=28, hkv=4, d=128, dtype=di.BF16, seed=5)
+    shape = di.Shape("big_q", L_d=1000, L_q=8192, n=100, hq=28, hkv=4, d=128, dtype=di.BF16, seed=5)
     batch = di.make_batch([shape])
     buf = LayerBuffers(batch.arrays, batch.cu_doc, batch.cu_q, batch.cu_imp, 28, 4, 128)
     assert daf.daf_layer_workspace_size(buf.cfg, buf.batch) > daf.daf_layer_noalloc_max_bytes()
