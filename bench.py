@@ -7,16 +7,18 @@ both stages write their rows into the hidden states in their epilogues). At
 least W untimed warmup steps (and at least --warmup-ms of GPU time, so that the
 shader clock has reached its level under sustained load), then exactly K timed
 steps between device synchronisations. Several copies of the inputs are
-used in rotation so that consecutive steps do not find their data in the
-256 MB Infinity Cache.
+used in rotation; together they touch far more than the 256 MB Infinity Cache
+(MALL), so consecutive steps do not find their data there.
 
-A second timed loop calls the stages one by one with HIP events between them
-(on the stream the kernels run on) for per-stage times, TFLOP/s, TB/s and the
-roofline fraction of the dominant kernel (stage 1). Its HBM traffic comes from
-the committed rocprofv3 counter summary when that summary was taken on the
-current attention sources (their SHA-256 is recorded there), else it is null.
-The CPU oracle is timed on the host on a bounded sample of the same layer
-(``cpu_baseline``).
+A second timed loop calls the stages one by one with HIP events around each
+call (on the stream the kernels run on) for per-stage times, TFLOP/s, TB/s and
+the roofline fraction of the dominant kernel (stage 1). Before each timed call
+a 512 MiB scratch buffer is read and written, which evicts the MALL, and a GPU
+spin follows so that the events and the call are queued before the GPU reaches
+them. HBM traffic and kernel-trace averages come from the committed rocprofv3
+summaries when they were taken on the current attention sources (their SHA-256
+is recorded there), else they are null. The CPU oracle is timed on the host on
+bounded samples of every workload (``cpu_baseline``).
 
 Prints one JSON line.
 """
@@ -39,17 +41,21 @@ METRIC = "DAF per-layer attention µs at L_d=32k,r=0.15; stage TFLOP/s + HBM TB/
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_stage1_qwen7b_32k_pmc.md")
-# sources whose change invalidates counter-measured traffic of the attention kernels
-# What determines a standalone stage-1 launch: the kernel and its grid, the
-# launch structures, the compile flags, and the host functions that build the
-# stage-1 work table. A traffic record taken on other versions of these is not
-# used.
-ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_21599_amd", "csrc", f) for f in ("attn_bf16.hip", "daf_internal.h")] + [
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_qwen7b_32k_pmc.md")
+TRACE_SUMMARY = os.path.join(ROOT, "profiles", "attn_layer_qwen7b_32k_kernel_trace.md")
+EVICT_MIB = 512  # scratch streamed through before each timed stage call (MALL is 256 MB)
+# What determines a standalone stage-1 or stage-2 launch: the kernels and their
+# grids, the launch structures, the compile flags, and the host functions that
+# build the work tables, plan the key splits and launch the merge. A profile
+# record taken on other versions of these is not used.
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_21599_amd", "csrc", f)
+                for f in ("attn_bf16.hip", "attn.hip", "daf_internal.h")] + [
     os.path.join(ROOT, "paper_2607_21599_amd", "build.py")]
 ATTN_HOST = os.path.join(ROOT, "paper_2607_21599_amd", "csrc", "api.hip")
 ATTN_HOST_FUNCTIONS = ("AttnEntry self_entry(", "int entry_groups(", "daf_status_t run_entries(",
-                       "void add_self_entries(")
+                       "void add_self_entries(", "bool packed_qdoc(", "int qdoc_blocks(",
+                       "std::vector<Split> plan_splits(", "WsLayout ws_layout(", "AttnEntry qdoc_entry(",
+                       "daf_status_t qdoc_entries(", "daf_status_t run_merge(")
 
 
 def _function_text(src: str, head: str) -> str:
@@ -75,25 +81,29 @@ def attn_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
-    """Counter-measured HBM bytes per stage-1 launch from the committed
-    summary, or None if it is absent, for another workload, or was taken on
-    other attention sources."""
+def profile_record(path: str, tag: str, workload: str) -> dict:
+    """The `tag:` line of a committed profile summary as a dict, or {} if the
+    summary is absent, for another workload, or was taken on other attention
+    sources."""
     try:
-        with open(TRAFFIC_SUMMARY) as fh:
+        with open(path) as fh:
             lines = fh.read().splitlines()
     except OSError:
-        return None
+        return {}
     fields = {}
     for ln in lines:
-        if ln.startswith("traffic-record:"):
+        if ln.startswith(tag + ":"):
             for kv in ln.split(":", 1)[1].split():
                 k, _, v = kv.partition("=")
                 fields[k] = v
     if fields.get("workload") != workload or fields.get("sources_sha256") != attn_source_hash():
-        return None
+        return {}
+    return fields
+
+
+def record_number(rec: dict, key: str):
     try:
-        return int(fields["stage1_hbm_bytes_per_launch"])
+        return float(rec[key])
     except (KeyError, ValueError):
         return None
 
@@ -127,15 +137,19 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
-    """The oracle on every stride1-th stage-1 row and every stride2-th stage-2
-    row (plus the full hybrid-cache build and fusion), scaled to the layer."""
+def oracle_layer_us(batch, stride1: int, stride2: int, requests=None):
+    """Oracle time of one layer in µs: the full hybrid-cache build and fusion,
+    and the attention of every stride1-th stage-1 row and every stride2-th
+    stage-2 row of the chosen requests, each attention time scaled by total
+    over sampled rows. Returns (µs, stage-1 rows, stage-2 rows, threads)."""
     import oracle
     orc = oracle.get()
     w = di.raw_to_f32
     t_total = 0.0
     rows_done = [0, 0]
     for b, s in enumerate(batch.shapes):
+        if requests is not None and b not in requests:
+            continue
         r = batch.request(b)
         sc = oracle.default_scale(s.d)
         rows1 = np.arange(0, s.n, stride1)
@@ -146,11 +160,11 @@ def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
                                r["v_q"], s.L_d)
         t_hyb = time.perf_counter() - t0
         t0 = time.perf_counter()
-        o1, _ = orc.stage1(q1, k1, v1, r["idx"], sc, rows1)
+        orc.stage1(q1, k1, v1, r["idx"], sc, rows1)
         t_s1 = time.perf_counter() - t0
         kf, vf, qq = w(kh), w(vh), w(r["q_q"])
         t0 = time.perf_counter()
-        o2, _ = orc.stage2(qq, kf, vf, s.L_d, sc, rows2)
+        orc.stage2(qq, kf, vf, s.L_d, sc, rows2)
         t_s2 = time.perf_counter() - t0
         t0 = time.perf_counter()
         orc.fuse_hidden(r["hidden"], r["idx"], r["q_imp"], r["q_q"], s.L_d)
@@ -158,17 +172,58 @@ def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
         t_total += t_hyb + t_fuse + t_s1 * s.n / max(1, len(rows1)) + t_s2 * s.L_q / max(1, len(rows2))
         rows_done[0] += len(rows1)
         rows_done[1] += len(rows2)
-    return dict(value=t_total * 1e6, unit="us", cores=orc.threads, kind="oracle", cpu=cpu_model(),
-                sample=(f"stage-1 rows 0::{stride1} ({rows_done[0]} rows) and stage-2 rows 0::{stride2} "
-                        f"({rows_done[1]} rows) of every request, full hybrid-cache build and fusion; "
+    return t_total * 1e6, rows_done[0], rows_done[1], orc.threads
+
+
+def cpu_baseline(batch, stride1: int, stride2: int) -> dict:
+    """The oracle on a row sample of the bench workload, scaled to the layer."""
+    us, n1, n2, threads = oracle_layer_us(batch, stride1, stride2)
+    return dict(value=us, unit="us", cores=threads, kind="oracle", cpu=cpu_model(),
+                sample=(f"stage-1 rows 0::{stride1} ({n1} rows) and stage-2 rows 0::{stride2} "
+                        f"({n2} rows) of every request, full hybrid-cache build and fusion; "
                         "attention times scaled by total/sampled rows"))
 
 
-def decoder_layer_section(s0, batch, spin_cycles: int, selection_us) -> dict:
+# The other workloads the oracle is timed on: (workload, stage-1 stride,
+# stage-2 stride, sampled requests or None for all). The batched workload is
+# timed on three of its eight requests, generated one at a time, and scaled by
+# the attention FLOP of all eight over those three.
+ORACLE_SAMPLES = [("tiny_f32_1k", 1, 1, None), ("qwen7b_6k", 2, 1, None), ("qwen7b_16k_r05", 4, 2, None),
+                  ("qwen7b_16k_r15", 8, 2, None), ("qwen7b_16k_r30", 16, 4, None),
+                  ("qwen7b_batch8", 16, 4, (0, 3, 7))]
+
+
+def cpu_baseline_configs() -> list:
+    out = []
+    for name, st1, st2, reqs in ORACLE_SAMPLES:
+        shapes = di.workload(name)
+        if reqs is None:
+            us, n1, n2, _ = oracle_layer_us(di.make_batch(shapes), st1, st2)
+            sample = f"stage-1 rows 0::{st1} ({n1}), stage-2 rows 0::{st2} ({n2}), scaled by total/sampled rows"
+        else:
+            us, n1, n2 = 0.0, 0, 0
+            for b in reqs:
+                u, a, c, _ = oracle_layer_us(di.make_batch([shapes[b]]), st1, st2)
+                us, n1, n2 = us + u, n1 + a, n2 + c
+            wall = work(shapes)
+            part = work([shapes[b] for b in reqs])
+            scale = (wall["stage1_flop"] + wall["stage2_flop"]) / (part["stage1_flop"] + part["stage2_flop"])
+            us *= scale
+            sample = (f"requests {', '.join(str(b) for b in reqs)} of {len(shapes)}: stage-1 rows 0::{st1} ({n1}), "
+                      f"stage-2 rows 0::{st2} ({n2}), scaled by total/sampled rows, then by the attention FLOP "
+                      f"of all requests over the sampled ones (x{scale:.2f})")
+        out.append({"workload": name, "us": us, "sample": sample})
+        print(f"[bench] oracle {name}: {us / 1e6:.2f} s per layer (estimated from a sample)", file=sys.stderr,
+              flush=True)
+    return out
+
+
+def decoder_layer_section(s0, batch, spin_cycles: int, selection_us, evict) -> dict:
     """One prefill decoder layer with Qwen2.5-7B-shaped synthetic weights:
     DAF (only the important and question rows, DAF attention on the hybrid
     cache) against full recomputation (every row, causal attention), each
-    call timed alone behind a GPU spin, and a 28-layer TTFT model from them."""
+    call timed alone behind a MALL eviction (`evict`) and a GPU spin, and a
+    28-layer TTFT model from them."""
     import torch
 
     import paper_2607_21599_amd as daf
@@ -212,6 +267,7 @@ def decoder_layer_section(s0, batch, spin_cycles: int, selection_us) -> dict:
         t = []
         for _ in range(c["reps"]):
             x.copy_(c["x0"])
+            evict()
             torch.cuda._sleep(spin_cycles)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
@@ -257,7 +313,15 @@ def main():
     ap.add_argument("--no-layer", action="store_true",
                     help="skip the decoder-layer section (projections, norms and MLP around the attention)")
     ap.add_argument("--no-patterns", action="store_true",
-                    help="skip the comparison patterns (CacheBlend-style and full recomputation attention)")
+                    help="skip the selection call and the comparison patterns (CacheBlend-style and full "
+                         "recomputation attention)")
+    ap.add_argument("--no-lq32", action="store_true", help="skip stage 2 at L_q = 32")
+    ap.add_argument("--no-oracle-configs", action="store_true",
+                    help="time the CPU oracle on the bench workload only")
+    ap.add_argument("--evict", choices=("read", "write"), default="read",
+                    help="how the 512 MiB scratch evicts the MALL before each timed call: read it (the MALL "
+                         "then holds clean lines), or read and write it (dirty lines, whose write-back then "
+                         "competes with the timed call's reads)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a known-size "
                          "kernel that calibrates HBM byte counters)")
@@ -318,13 +382,45 @@ def main():
     t1.record()
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / args.steps
+    wk0 = work(shapes)
+    step_touch = (wk0["gather_bytes"] + wk0["fuse_kv_bytes"] + wk0["stage1_bytes"] + wk0["stage2_bytes"]
+                  + wk0["fuse_hidden_bytes"])
     print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
-    # Per-stage times: events around each stage call on the launch stream. A
-    # host call takes longer than the shorter kernels, so a GPU spin is queued
-    # before each timed call: the events and the call are all enqueued before
-    # the GPU reaches them, and the event pair measures the call's GPU time.
-    # The calls are idempotent (same inputs, same outputs).
+    # Per-stage times: events around each stage call on the launch stream.
+    # Before each timed call a 512 MiB scratch buffer is read and written
+    # (evicting the 256 MB MALL, so the call reads its inputs from HBM), then a
+    # GPU spin is queued: a host call takes longer than the shorter kernels, and
+    # the spin lets the events and the call be enqueued before the GPU reaches
+    # them, so the event pair measures the call's GPU time. The calls are
+    # idempotent (same inputs, same outputs).
+    evict = torch.zeros(EVICT_MIB << 20, dtype=torch.uint8, device="cuda")
+    evict_sum = torch.zeros(1, dtype=torch.int64, device="cuda")
+    spin_cycles = 400_000  # ~0.2 ms at the MI355X shader clock, longer than a host call
+
+    def evict_mall():
+        if args.evict == "write":
+            evict.add_(1)
+        else:
+            torch.sum(evict.view(torch.int64), dim=0, keepdim=True, out=evict_sum)
+
+    def timed_calls(fn, n):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for i in range(n):
+            evict_mall()
+            torch.cuda._sleep(spin_cycles)
+            ev[i][0].record()
+            fn(i)
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+
+    # the floor of this timing: an event pair around nothing
+    event_floor = float(np.mean(timed_calls(lambda i: None, args.steps)))
+    # the same step, one call at a time, each after a MALL eviction
+    t_cold = timed_calls(step, args.steps)
+    print(f"[bench] step after MALL eviction: {np.mean(t_cold):.1f} us", file=sys.stderr, flush=True)
+
     names = ["gather", "fuse_kv", "stage1", "stage2", "fuse_hidden"]
     calls = {
         "gather": lambda j: bufs[j].gather_hidden(gath[j]),
@@ -333,19 +429,11 @@ def main():
         "stage2": lambda j: bufs[j].stage2(),
         "fuse_hidden": lambda j: bufs[j].fuse_hidden(),
     }
-    spin_cycles = 400_000  # ~0.2 ms at the MI355X shader clock, longer than a host call
     stage_us, stage_pct = {}, {}
     for n in names:
         calls[n](0)
         torch.cuda.synchronize()
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-        for i in range(args.steps):
-            torch.cuda._sleep(spin_cycles)
-            ev[i][0].record()
-            calls[n](i % len(bufs))
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        t_us = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+        t_us = timed_calls(lambda i: calls[n](i % len(bufs)), args.steps)
         stage_us[n] = float(np.mean(t_us))
         stage_pct[n] = [float(x) for x in np.percentile(t_us, [10, 50, 90])]
     wk = work(shapes)
@@ -383,17 +471,36 @@ def main():
         # roofline time of the bound that applies, over the measured time
         t_floor = max(st["flop"] / (peak_mma * 1e12), st["bytes"] / (PEAK_HBM_GBS * 1e9))
         st["roofline_frac"] = t_floor / (st["us"] * 1e-6)
+    # Kernel-trace averages and counter-measured HBM bytes of the standalone
+    # launches, from the committed rocprofv3 summaries of this workload (null
+    # when those were taken on other attention sources).
+    trace = profile_record(TRACE_SUMMARY, "trace-record", args.workload)
+    traffic = profile_record(TRAFFIC_SUMMARY, "traffic-record", args.workload)
     s1 = stages["stage1_imp_self_attn"]
+    s1_trace_us = record_number(trace, "stage1_avg_us")
+    s1_traffic = record_number(traffic, "stage1_hbm_bytes_per_launch")
     roofline = dict(bound="mfma", kernel="attn_bf16_kernel<128,0> (stage 1, daf_imp_self_attn)",
                     achieved=s1["TFLOPs"], peak=peak_mma, unit="TFLOP/s", frac=s1["TFLOPs"] / peak_mma,
-                    traffic=measured_traffic(args.workload), traffic_unit="bytes per launch (HBM, counters)",
-                    flop_per_launch=wk["stage1_flop"], launch_us=s1["us"])
+                    traffic=int(s1_traffic) if s1_traffic else None,
+                    traffic_unit="bytes per launch (HBM, counters)",
+                    flop_per_launch=wk["stage1_flop"], launch_us=s1["us"], launch_us_rocprof=s1_trace_us,
+                    frac_rocprof=(tflops(wk["stage1_flop"], s1_trace_us) / peak_mma) if s1_trace_us else None,
+                    frac_note="frac: HIP-event time of the standalone call in this run; frac_rocprof: the "
+                              "kernel's average duration in the committed kernel trace")
+    s2 = stages["stage2_qdoc_attn"]
+    s2_trace = [record_number(trace, k) for k in ("stage2_avg_us", "merge_avg_us")]
+    s2_bytes = [record_number(traffic, k) for k in ("stage2_hbm_bytes_per_launch", "merge_hbm_bytes_per_launch")]
+    s2["kernel_us_rocprof"] = sum(s2_trace) if None not in s2_trace else None
+    s2["hbm_bytes_counted"] = int(sum(s2_bytes)) if None not in s2_bytes else None
+    s2["counted_over_algorithmic"] = (sum(s2_bytes) / s2["bytes"]) if None not in s2_bytes else None
+    s2["hbm_bytes_counted_split"] = ({"attention": int(s2_bytes[0]), "merge": int(s2_bytes[1])}
+                                     if None not in s2_bytes else None)
 
     # Stage 2 in its bandwidth-bound regime: the same layer with a 32-token
     # question (7 query rows per cached K/V byte, below the MFMA/HBM ridge),
-    # timed alone like the stage calls above, three input copies in rotation.
+    # timed alone like the stage calls above (MALL evicted before each call).
     stage2_lq32 = None
-    if not args.no_patterns and args.workload == "qwen7b_32k":
+    if not args.no_lq32 and args.workload == "qwen7b_32k":
         print("[bench] stage 2 at L_q = 32", file=sys.stderr, flush=True)
         shp32 = di.workload("qwen7b_32k_lq32")
         b32 = di.make_batch(shp32)
@@ -403,29 +510,30 @@ def main():
             bb.fuse_kv()
         bufs32[0].stage2()
         torch.cuda.synchronize()
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-        for i in range(args.steps):
-            torch.cuda._sleep(spin_cycles)
-            ev[i][0].record()
-            bufs32[i % len(bufs32)].stage2()
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        us32 = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        us32 = float(np.mean(timed_calls(lambda i: bufs32[i % len(bufs32)].stage2(), args.steps)))
         wk32 = work(shp32)
         t_hbm = wk32["stage2_bytes"] / (PEAK_HBM_GBS * 1e9)
         t_mma = wk32["stage2_flop"] / (peak_mma * 1e12)
+        tr32 = [record_number(trace, k) for k in ("stage2_lq32_avg_us", "merge_lq32_avg_us")]
+        by32 = [record_number(traffic, k) for k in ("stage2_lq32_hbm_bytes_per_launch",
+                                                     "merge_lq32_hbm_bytes_per_launch")]
         stage2_lq32 = {"workload": "qwen7b_32k_lq32", "L_q": shp32[0].L_q, "us": us32,
                        "bytes": wk32["stage2_bytes"], "GBps": gbs(wk32["stage2_bytes"], us32),
                        "hbm_frac": gbs(wk32["stage2_bytes"], us32) / PEAK_HBM_GBS,
                        "flop": wk32["stage2_flop"], "TFLOPs": tflops(wk32["stage2_flop"], us32),
                        "floor_us": {"hbm": t_hbm * 1e6, "mfma": t_mma * 1e6},
-                       "roofline_frac": max(t_hbm, t_mma) / (us32 * 1e-6)}
+                       "roofline_frac": max(t_hbm, t_mma) / (us32 * 1e-6),
+                       "kernel_us_rocprof": sum(tr32) if None not in tr32 else None,
+                       "hbm_frac_rocprof": (gbs(wk32["stage2_bytes"], sum(tr32)) / PEAK_HBM_GBS
+                                            if None not in tr32 else None),
+                       "hbm_bytes_counted": int(sum(by32)) if None not in by32 else None,
+                       "counted_over_algorithmic": (sum(by32) / wk32["stage2_bytes"]) if None not in by32 else None}
         del bufs32, b32
 
     selection = None
     if not args.no_patterns:
         # The step before the path: choosing the important tokens from the KV
-        # deviation over three selection layers (same spin + event timing).
+        # deviation over three selection layers (same eviction + spin + event timing).
         print("[bench] important-token selection", file=sys.stderr, flush=True)
         import paper_2607_21599_amd as daf_mod
         from paper_2607_21599_amd.tensors import to_device
@@ -446,15 +554,7 @@ def main():
 
         run_sel()
         torch.cuda.synchronize()
-        reps = 10
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-        for i in range(reps):
-            torch.cuda._sleep(spin_cycles)
-            ev[i][0].record()
-            run_sel()
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        sel_us = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+        sel_us = float(np.mean(timed_calls(lambda i: run_sel(), 10)))
         eb = 2 if s0.dtype == di.BF16 else 4
         sel_bytes = 2 * n_sel_layers * n_doc * s0.hkv * s0.d * eb + 4 * n_doc + 4 * int(batch.cu_imp[-1])
         selection = {"us": sel_us, "layers": n_sel_layers, "bytes": sel_bytes, "GBps": gbs(sel_bytes, sel_us),
@@ -466,7 +566,7 @@ def main():
         # The schemes the Complexity Analysis compares DAF with, as attention on
         # the same GPU: the CacheBlend pattern (important and question rows over
         # the whole hybrid cache, causal by position) and full recomputation
-        # (every token over its prefix). Same spin + event timing per call.
+        # (every token over its prefix). Same eviction + spin + event timing.
         print("[bench] comparison patterns", file=sys.stderr, flush=True)
         pb = bufs[0]
         pb.fuse_kv()
@@ -475,15 +575,7 @@ def main():
         for n, fn in (("cacheblend", pb.cacheblend), ("full_recompute", pb.full_recompute)):
             fn()
             torch.cuda.synchronize()
-            reps = 5
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-            for i in range(reps):
-                torch.cuda._sleep(spin_cycles)
-                ev[i][0].record()
-                fn()
-                ev[i][1].record()
-            torch.cuda.synchronize()
-            pat_us[n] = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+            pat_us[n] = float(np.mean(timed_calls(lambda i: fn(), 5)))
         idx = batch.request(0)["idx"].astype(np.int64)
         pos = np.concatenate([idx, s0.L_d + np.arange(s0.L_q)])
         f_cb = 4 * s0.d * s0.hq * int((pos + 1).sum())
@@ -504,7 +596,7 @@ def main():
     layer = None
     if not args.no_layer and len(shapes) == 1 and s0.dtype == di.BF16:
         print("[bench] decoder layer: DAF vs full recomputation", file=sys.stderr, flush=True)
-        layer = decoder_layer_section(s0, batch, spin_cycles, selection["us"] if selection else None)
+        layer = decoder_layer_section(s0, batch, spin_cycles, selection["us"] if selection else None, evict_mall)
 
     out = {
         "metric": METRIC, "value": ms_per_step * 1e3, "unit": "us", "n_gpus": 1, "steps": args.steps,
@@ -516,6 +608,15 @@ def main():
                    "n_imp": [s.n for s in shapes] if len(shapes) > 1 else s0.n,
                    "q_heads": s0.hq, "kv_heads": s0.hkv, "head_dim": s0.d, "requests": len(shapes),
                    "step": "gather + daf_layer_attn", "input_copies": len(bufs)},
+        "mall": {"value": f"{args.steps} steps back to back, {len(bufs)} input copies in rotation; one copy "
+                          f"touches {step_touch / 1e6:.0f} MB per step, so consecutive steps sharing a copy are "
+                          f"{(len(bufs) - 1) * step_touch / 1e6:.0f} MB of other traffic apart (MALL 256 MB)",
+                 "per_call": f"{EVICT_MIB} MiB scratch {'read' if args.evict == 'read' else 'read and written'} "
+                             "before each timed call (stages, step_us_mall_evicted, stage2_lq32, selection, "
+                             "comparison, decoder_layer), outside the events",
+                 "evict": args.evict},
+        "event_floor_us": event_floor,
+        "step_us_mall_evicted": float(np.mean(t_cold)),
         "layer_attn_us_sum_of_stages": sum(stage_us[n] for n in names[1:]),
         "stages": stages,
         "roofline": roofline,
@@ -531,6 +632,8 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(batch, args.cpu_stride1, args.cpu_stride2)
+        if not args.no_oracle_configs:
+            out["cpu_baseline"]["other_workloads"] = cpu_baseline_configs()
     print(json.dumps(out), flush=True)
 
 
