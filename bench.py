@@ -436,7 +436,20 @@ def main():
         t_us = timed_calls(lambda i: calls[n](i % len(bufs)), args.steps)
         stage_us[n] = float(np.mean(t_us))
         stage_pct[n] = [float(x) for x in np.percentile(t_us, [10, 50, 90])]
+    # Reference for the row kernels: a plain contiguous device copy moving the
+    # same bytes (read + write) as each of them, timed the same way.
     wk = work(shapes)
+    copy_ref = {}
+    for name, nbytes in (("gather", wk["gather_bytes"]), ("fuse_kv", wk["fuse_kv_bytes"]),
+                         ("fuse_hidden", wk["fuse_hidden_bytes"])):
+        half = (nbytes // 2 + 15) // 16 * 16
+        src = torch.empty(half, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        t_copy = float(np.mean(timed_calls(lambda i: dst.copy_(src), args.steps)))
+        copy_ref[name] = {"bytes": 2 * half, "us": t_copy, "GBps": 2 * half / (t_copy * 1e-6) / 1e9}
+        del src, dst
     peak_mma = PEAK_BF16_TFLOPS if s0.dtype == di.BF16 else PEAK_F32_TFLOPS
 
     def tflops(f, us):
@@ -464,6 +477,7 @@ def main():
         stages[k]["us_p10_p50_p90"] = stage_pct[n]
     for k in ("gather", "fuse_kv", "fuse_hidden"):
         stages[k]["hbm_frac"] = stages[k]["GBps"] / PEAK_HBM_GBS
+        stages[k]["plain_copy_same_bytes"] = copy_ref[k]
     for k in ("stage1_imp_self_attn", "stage2_qdoc_attn"):
         st = stages[k]
         st["mfma_frac"] = st["TFLOPs"] / peak_mma
@@ -487,6 +501,14 @@ def main():
                     frac_rocprof=(tflops(wk["stage1_flop"], s1_trace_us) / peak_mma) if s1_trace_us else None,
                     frac_note="frac: HIP-event time of the standalone call in this run; frac_rocprof: the "
                               "kernel's average duration in the committed kernel trace")
+    for k, rk in (("gather", "gather"), ("fuse_kv", "fuse_kv"), ("fuse_hidden", "fuse_hidden")):
+        t_k = record_number(trace, rk + "_avg_us")
+        b_k = record_number(traffic, rk + "_hbm_bytes_per_launch")
+        stages[k]["kernel_us_rocprof"] = t_k
+        stages[k]["hbm_frac_rocprof"] = gbs(stages[k]["bytes"], t_k) / PEAK_HBM_GBS if t_k else None
+        stages[k]["hbm_bytes_counted"] = int(b_k) if b_k else None
+    s1["kernel_us_rocprof"] = s1_trace_us
+    s1["hbm_bytes_counted"] = int(s1_traffic) if s1_traffic else None
     s2 = stages["stage2_qdoc_attn"]
     s2_trace = [record_number(trace, k) for k in ("stage2_avg_us", "merge_avg_us")]
     s2_bytes = [record_number(traffic, k) for k in ("stage2_hbm_bytes_per_launch", "merge_hbm_bytes_per_launch")]
