@@ -57,3 +57,32 @@ def test_bytes_at_32k():
     assert w["gather_bytes"] == 2 * n * q_row
     assert w["fuse_hidden_bytes"] == 2 * (n + L_q) * q_row
     assert w["fuse_kv_bytes"] == 2 * (n + L_q) * 2 * kv_row
+
+
+def test_profile_records_used_only_for_the_same_sources_and_workload(tmp_path):
+    """The bench takes kernel times and HBM bytes from a committed profile
+    summary only when its record line names the workload and the SHA-256 of
+    the current attention sources."""
+    sha = bench.attn_source_hash()
+    f = tmp_path / "summary.md"
+    f.write_text("# title\n\nsome text\n"
+                 f"traffic-record: workload=qwen7b_32k stage1_hbm_bytes_per_launch=123 sources_sha256={sha}\n")
+    rec = bench.profile_record(str(f), "traffic-record", "qwen7b_32k")
+    assert bench.record_number(rec, "stage1_hbm_bytes_per_launch") == 123.0
+    assert bench.record_number(rec, "absent_key") is None
+    assert bench.profile_record(str(f), "traffic-record", "qwen7b_6k") == {}
+    assert bench.profile_record(str(f), "trace-record", "qwen7b_32k") == {}
+    f.write_text(f"traffic-record: workload=qwen7b_32k stage1_hbm_bytes_per_launch=123 sources_sha256={'0' * 64}\n")
+    assert bench.profile_record(str(f), "traffic-record", "qwen7b_32k") == {}
+    assert bench.profile_record(str(tmp_path / "missing.md"), "traffic-record", "qwen7b_32k") == {}
+
+
+def test_committed_profiles_match_the_sources():
+    """The committed summaries were taken on the attention sources in the tree
+    (otherwise the bench reports their figures as null)."""
+    trace = bench.profile_record(bench.TRACE_SUMMARY, "trace-record", "qwen7b_32k")
+    traffic = bench.profile_record(bench.TRAFFIC_SUMMARY, "traffic-record", "qwen7b_32k")
+    for key in ("stage1_avg_us", "stage2_avg_us", "merge_avg_us", "gather_avg_us"):
+        assert bench.record_number(trace, key) is not None, key
+    for key in ("stage1_hbm_bytes_per_launch", "stage2_hbm_bytes_per_launch", "merge_hbm_bytes_per_launch"):
+        assert bench.record_number(traffic, key) is not None, key
