@@ -80,3 +80,37 @@ def test_layer_every_row(workload, q_scale):
     idx_t = torch.from_numpy(r["idx"].astype(np.int64)).cuda()
     assert torch.equal(buf["hidden"][idx_t].view(-1), buf["o_imp"].reshape(-1))
     assert torch.equal(buf["hidden"][s.L_d:].reshape(-1), buf["o_q"].reshape(-1))
+
+
+def test_batch_every_row():
+    """Eight ragged requests (L_d 4k-32k, L_q 32-256) in one daf_layer_attn
+    call, every row of every request against the oracle: request offsets,
+    per-request key splits and the stage-1 job order across requests."""
+    from paper_2607_21599_amd.tensors import LayerBuffers
+    batch = di.make_batch(di.workload("qwen7b_batch8"))
+    s0 = batch.shapes[0]
+    print("[full-oracle] qwen7b_batch8: daf_layer_attn", flush=True)
+    buf = LayerBuffers(batch.arrays, batch.cu_doc, batch.cu_q, batch.cu_imp, s0.hq, s0.hkv, s0.d)
+    buf.layer()
+    torch.cuda.synchronize()
+    o_imp, o_q = _f32(buf["o_imp"]), _f32(buf["o_q"])
+    lse_imp, lse_q = _f32(buf["lse_imp"]).T, _f32(buf["lse_q"]).T
+    k_cache, v_cache = _raw(buf["k_cache"]), _raw(buf["v_cache"])
+    for b, s in enumerate(batch.shapes):
+        print(f"[full-oracle] qwen7b_batch8 request {b}: oracle on all {s.n} + {s.L_q} rows", flush=True)
+        r = batch.request(b)
+        ref = oracle_request(r)
+        i0, i1, q0, q1 = batch.cu_imp[b], batch.cu_imp[b + 1], batch.cu_q[b], batch.cu_q[b + 1]
+        t0, t1 = batch.cu_tok[b], batch.cu_tok[b + 1]
+        what = f"batch8 request {b}"
+        assert_attn_close(o_imp[i0:i1], ref["o_imp"], di.BF16, f"{what} stage1")
+        assert_lse_close(lse_imp[i0:i1], ref["lse_imp"], di.BF16, f"{what} stage1 lse")
+        assert_attn_close(o_q[q0:q1], ref["o_q"], di.BF16, f"{what} stage2")
+        assert_lse_close(lse_q[q0:q1], ref["lse_q"], di.BF16, f"{what} stage2 lse")
+        for name, g, e in (("stage1", o_imp[i0:i1], ref["o_imp"]), ("stage2", o_q[q0:q1], ref["o_q"])):
+            num = np.sqrt(((g.astype(np.float64) - e) ** 2).sum(axis=(1, 2)))
+            den = np.sqrt((e ** 2).sum(axis=(1, 2)))
+            worst = int(np.argmax(num / den))
+            assert float(num[worst] / den[worst]) <= 2e-2, f"{what} {name} row {worst}"
+        assert np.array_equal(k_cache[t0:t1], ref["k_hyb"]), what
+        assert np.array_equal(v_cache[t0:t1], ref["v_hyb"]), what
