@@ -345,6 +345,67 @@ def pin_brute_force_subsets(orc):
             _close(out["o_q"], ref, what=f"subset {sub} stage2")
 
 
+def _py_causal_attention(q, k, v, scale, limits, group):
+    """Attention written out in plain Python floats (fp64, math module only):
+    row i of query head h sees keys 0 .. limits[i] of KV head h // group.
+    q: [rows][Hq][D], k, v: [keys][Hkv][D] nested lists. Returns (o, lse)."""
+    d = len(q[0][0])
+    out, lse = [], []
+    for i, qi in enumerate(q):
+        o_row, l_row = [], []
+        for h, qh in enumerate(qi):
+            g = h // group
+            s = [scale * math.fsum(qh[t] * k[j][g][t] for t in range(d)) for j in range(limits[i] + 1)]
+            m = max(s)
+            e = [math.exp(x - m) for x in s]
+            z = math.fsum(e)
+            o_row.append([math.fsum(e[j] * v[j][g][t] for j in range(len(e))) / z for t in range(d)])
+            l_row.append(m + math.log(z))
+        out.append(o_row)
+        lse.append(l_row)
+    return out, lse
+
+
+def pin_pure_python_subsets(orc):
+    """Every non-empty important subset of a 7-token document set with a
+    3-token question (GQA 2:1), recomputed by a second implementation in pure
+    Python floats (no numpy, no torch): the hybrid cache by list assignment,
+    stage 1 over the chosen tokens, stage 2 over [hybrid docs; question]. The
+    C oracle must agree to 1e-12 relative, outputs and LSE."""
+    rng = _rng(26)
+    L_d, L_q, hq, hkv, d = 7, 3, 4, 2, 5
+    base = _sparse_layer_inputs(rng, L_d, L_q, L_d, hq, hkv, d, idx=np.arange(L_d))
+    scale = 0.45
+    to_list = lambda a: np.asarray(a, np.float64).tolist()
+    k_cache, v_cache = to_list(base["k_cache"]), to_list(base["v_cache"])
+    q_q, k_q, v_q = to_list(base["q_q"]), to_list(base["k_q"]), to_list(base["v_q"])
+
+    def rel(a, b, what):
+        a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+        assert a.shape == b.shape, what
+        err = float(np.max(np.abs(a - b) / np.maximum(np.abs(b), 1e-300)))
+        assert err <= 1e-12, f"{what}: relative error {err:.3g}"
+
+    for m in range(1, L_d + 1):
+        for sub in itertools.combinations(range(L_d), m):
+            x = dict(base)
+            x["idx"] = np.array(sub)
+            for key in ("q_imp", "k_imp", "v_imp"):
+                x[key] = base[key][:m]
+            out = orc.layer(scale=scale, L_d=L_d, **x)
+            q_imp, k_imp, v_imp = to_list(x["q_imp"]), to_list(x["k_imp"]), to_list(x["v_imp"])
+            o1, l1 = _py_causal_attention(q_imp, k_imp, v_imp, scale, list(range(m)), hq // hkv)
+            kh = [row[:] for row in k_cache[:L_d]] + k_q
+            vh = [row[:] for row in v_cache[:L_d]] + v_q
+            for i, t in enumerate(sub):
+                kh[t], vh[t] = k_imp[i], v_imp[i]
+            o2, l2 = _py_causal_attention(q_q, kh, vh, scale, [L_d + j for j in range(L_q)], hq // hkv)
+            rel(out["o_imp"], o1, f"subset {sub} stage1")
+            rel(out["lse_imp"], l1, f"subset {sub} stage1 lse")
+            rel(out["o_q"], o2, f"subset {sub} stage2")
+            rel(out["lse_q"], l2, f"subset {sub} stage2 lse")
+
+
 def pin_full_recompute_patterns(orc):
     """Comparison pattern 1 (full recomputation): causal attention over every
     token of the sequence, equal to torch's causal SDPA (GQA 7:1)."""
@@ -449,6 +510,7 @@ ALL_PINS = [
     pin_stage1_position_order, pin_hybrid_cache, pin_stage2_concat, pin_constant_values,
     pin_zero_queries, pin_gqa_groups, pin_needle, pin_probabilities, pin_layer_independence,
     pin_layer_full_recompute, pin_gather_scatter, pin_fuse_rows, pin_brute_force_subsets,
+    pin_pure_python_subsets,
     pin_full_recompute_patterns, pin_cacheblend_rows, pin_position_zero_queries,
     pin_selection_brute_force, pin_selection_invariants,
 ]
